@@ -1,0 +1,417 @@
+/*
+ * Plain CPU oracle for the sparse-selection hot path of append prefill.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test-suite, the smoke check and the
+ * CPU-baseline leg of the benchmark load this file's library.  It shares no
+ * code, header, table or helper with the HIP library: every value here is
+ * computed from the definitions, in double precision for floating point, with
+ * scalar loops and no blocking.  OpenMP splits independent query rows only.
+ *
+ * Sources (section / equation of the paper):
+ *   - selection of k history tokens per appended token by an indexer: Eq. (1),
+ *     Sec. "Sparse Attention", prefill phase; appended tokens' own indexer keys
+ *     are candidates too (same passage).  The indexer's formula is not printed
+ *     in the paper (it defers to the model's technical report); the reading used
+ *     is the lightning-indexer form: per query token t, heads h with weights
+ *     w[t,h] >= 0, one indexer key per token shared by all heads,
+ *         S[t,s] = sq[t] * sk[s] * sum_h w[t,h] * max(0, q[t,h,:] . kI[s,:]),
+ *     over candidates s in [0, M+t] (self included); later positions are -inf.
+ *   - union of the per-token selections loaded before attention: same
+ *     section, the paragraph after Eq. (1).
+ *   - predicted union and corrective reads S \ S_hat: Eq. (2) and the
+ *     paragraph after it, Sec. "KV Selection Prediction"; recall and precision
+ *     as defined under "Model-aligned prediction distance".
+ *   - read packing: maximal runs of selected, physically adjacent blocks,
+ *     address-ordered, never including unselected blocks: Sec. "Best-effort
+ *     read packing".  Runs are additionally split from their low end into
+ *     pieces of at most max_run pages.
+ *   - sparse attention over the selected tokens only: the paragraph after
+ *     Eq. (1) (KV of the selected tokens feed core attention).
+ *
+ * Every function returns 0 on success and a negative value on bad arguments.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define JO_F32 0
+#define JO_BF16 1
+#define JO_FP8 2
+
+/* OCP fp8 e4m3fn: 1 sign, 4 exponent bits (bias 7), 3 mantissa bits.
+ * Exponent field 0 is subnormal (m * 2^-9); S.1111.111 is NaN; no infinities. */
+double jo_fp8_e4m3fn_value(uint8_t b)
+{
+    int sign = (b >> 7) & 1;
+    int e = (b >> 3) & 15;
+    int m = b & 7;
+    double v;
+    if (e == 15 && m == 7)
+        return NAN;
+    if (e == 0)
+        v = ldexp((double)m, -9);
+    else
+        v = ldexp(1.0 + m / 8.0, e - 7);
+    return sign ? -v : v;
+}
+
+/* bf16: the upper 16 bits of an IEEE binary32 value. */
+double jo_bf16_value(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+static double elem(const void *base, int dt, int64_t i)
+{
+    switch (dt) {
+    case JO_F32: return (double)((const float *)base)[i];
+    case JO_BF16: return jo_bf16_value(((const uint16_t *)base)[i]);
+    default: return jo_fp8_e4m3fn_value(((const uint8_t *)base)[i]);
+    }
+}
+
+/* Session of a global query row: q_start is the prefix sum of new lengths. */
+static int session_of(int nseq, const int32_t *q_start, int row)
+{
+    int b = 0;
+    while (b + 1 < nseq && q_start[b + 1] <= row)
+        b++;
+    return b;
+}
+
+static int64_t key_base(const int32_t *q_start, const int32_t *hist_len, int b)
+{
+    int64_t base = 0;
+    for (int j = 0; j < b; j++)
+        base += (int64_t)hist_len[j] + (q_start[j + 1] - q_start[j]);
+    return base;
+}
+
+/*
+ * Indexer scores for a subset of query rows.
+ * q [total_q, H, d] (dtype q_dt), q_scale [total_q] or NULL (= 1);
+ * kI [total_ctx, d] (dtype k_dt), rows of session b start at the sum of the
+ * earlier sessions' M_b + N_b; k_scale [total_ctx] or NULL; w [total_q, H].
+ * out[r * out_ld + s] for s < out_ld: the score of candidate s, -inf beyond
+ * the causal limit M_b + i (and beyond the session's context).
+ */
+int jo_index_scores(int nseq, const int32_t *q_start, const int32_t *hist_len,
+                    const void *q, int q_dt, const float *q_scale,
+                    const void *kI, int k_dt, const float *k_scale,
+                    const float *w, int H, int d,
+                    int nrows, const int32_t *rows, double *out, int64_t out_ld)
+{
+    if (nseq < 1 || H < 1 || d < 1 || nrows < 0)
+        return -1;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int r = 0; r < nrows; r++) {
+        int g = rows[r];
+        if (g < 0 || g >= q_start[nseq]) {
+            bad = 1;
+            continue;
+        }
+        int b = session_of(nseq, q_start, g);
+        int i = g - q_start[b];
+        int64_t M = hist_len[b];
+        int64_t ctx = M + (q_start[b + 1] - q_start[b]);
+        int64_t kb = key_base(q_start, hist_len, b);
+        double sq = q_scale ? (double)q_scale[g] : 1.0;
+        double *qd = (double *)malloc(sizeof(double) * (size_t)H * d);
+        for (int64_t e = 0; e < (int64_t)H * d; e++)
+            qd[e] = elem(q, q_dt, (int64_t)g * H * d + e);
+        double *kd = (double *)malloc(sizeof(double) * (size_t)d);
+        for (int64_t s = 0; s < out_ld; s++) {
+            if (s > M + i || s >= ctx) {
+                out[(int64_t)r * out_ld + s] = -INFINITY;
+                continue;
+            }
+            for (int j = 0; j < d; j++)
+                kd[j] = elem(kI, k_dt, (kb + s) * d + j);
+            double acc = 0.0;
+            for (int h = 0; h < H; h++) {
+                double x = 0.0;
+                for (int j = 0; j < d; j++)
+                    x += qd[(int64_t)h * d + j] * kd[j];
+                double relu = x > 0.0 ? x : 0.0;
+                acc += (double)w[(int64_t)g * H + h] * relu;
+            }
+            double sk = k_scale ? (double)k_scale[kb + s] : 1.0;
+            out[(int64_t)r * out_ld + s] = sq * sk * acc;
+        }
+        free(kd);
+        free(qd);
+    }
+    return bad ? -2 : 0;
+}
+
+typedef struct {
+    double v;
+    int32_t idx;
+} jo_cand;
+
+/* Strict total order: larger score first, then smaller index. */
+static int cand_cmp(const void *a, const void *b)
+{
+    const jo_cand *x = (const jo_cand *)a, *y = (const jo_cand *)b;
+    if (x->v > y->v) return -1;
+    if (x->v < y->v) return 1;
+    return (x->idx > y->idx) - (x->idx < y->idx);
+}
+
+/*
+ * Top-k per query row (Eq. 1 selection).  scores[r * ld + s] holds row r's
+ * fp32 scores (r indexes the given rows); candidates are s in [0, M_b + i].
+ * out[r * k + j]: the selected ids in (score desc, id asc) order, then -1.
+ */
+int jo_topk(int nseq, const int32_t *q_start, const int32_t *hist_len,
+            int nrows, const int32_t *rows, const float *scores, int64_t ld,
+            int k, int32_t *out)
+{
+    if (nseq < 1 || k < 1 || nrows < 0)
+        return -1;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int r = 0; r < nrows; r++) {
+        int g = rows[r];
+        if (g < 0 || g >= q_start[nseq]) {
+            bad = 1;
+            continue;
+        }
+        int b = session_of(nseq, q_start, g);
+        int64_t n = (int64_t)hist_len[b] + (g - q_start[b]) + 1;
+        if (n > ld)
+            n = ld;
+        jo_cand *c = (jo_cand *)malloc(sizeof(jo_cand) * (size_t)(n > 0 ? n : 1));
+        for (int64_t s = 0; s < n; s++) {
+            double v = (double)scores[(int64_t)r * ld + s];
+            c[s].v = (v == 0.0) ? 0.0 : v; /* -0.0 compares equal to +0.0 */
+            c[s].idx = (int32_t)s;
+        }
+        qsort(c, (size_t)n, sizeof(jo_cand), cand_cmp);
+        for (int j = 0; j < k; j++)
+            out[(int64_t)r * k + j] = (j < n) ? c[j].idx : -1;
+        free(c);
+    }
+    return bad ? -2 : 0;
+}
+
+/*
+ * Page-demand set: A = { pt_b[s / page_size] : s selected by any row of
+ * session b, 0 <= s < min(limit_b, M_b + N_b) }, over a shared physical pool.
+ * topk_idx [total_q, k] session-local ids (others are padding);
+ * page_table [nseq, pt_ld]; limit [nseq] or NULL (= M_b, history only).
+ * bitmap [ceil(P/32)] (bit p%32 of word p/32); list ascending; *count.
+ */
+int jo_page_demand(int nseq, const int32_t *q_start, const int32_t *hist_len,
+                   const int32_t *topk_idx, int k,
+                   const int32_t *page_table, int pt_ld, int page_size,
+                   const int32_t *limit, int num_phys_pages,
+                   uint32_t *bitmap, int32_t *page_list, int32_t *count)
+{
+    if (nseq < 1 || k < 1 || page_size < 1 || num_phys_pages < 0)
+        return -1;
+    int nwords = (num_phys_pages + 31) / 32;
+    unsigned char *sel = (unsigned char *)calloc((size_t)num_phys_pages + 1, 1);
+    int bad = 0;
+    for (int b = 0; b < nseq; b++) {
+        int64_t ctx = (int64_t)hist_len[b] + (q_start[b + 1] - q_start[b]);
+        int64_t lim = limit ? limit[b] : hist_len[b];
+        if (lim > ctx)
+            lim = ctx;
+        for (int g = q_start[b]; g < q_start[b + 1]; g++) {
+            for (int j = 0; j < k; j++) {
+                int64_t s = topk_idx[(int64_t)g * k + j];
+                if (s < 0 || s >= lim)
+                    continue;
+                int64_t lp = s / page_size;
+                if (lp >= pt_ld) {
+                    bad = 1;
+                    continue;
+                }
+                int p = page_table[(int64_t)b * pt_ld + lp];
+                if (p < 0 || p >= num_phys_pages) {
+                    bad = 1;
+                    continue;
+                }
+                sel[p] = 1;
+            }
+        }
+    }
+    int c = 0;
+    for (int w = 0; w < nwords; w++)
+        bitmap[w] = 0;
+    for (int p = 0; p < num_phys_pages; p++) {
+        if (sel[p]) {
+            bitmap[p / 32] |= 1u << (p % 32);
+            page_list[c++] = p;
+        }
+    }
+    *count = c;
+    free(sel);
+    return bad ? -2 : 0;
+}
+
+static int bit_at(const uint32_t *bm, int p)
+{
+    return (int)((bm[p / 32] >> (p % 32)) & 1u);
+}
+
+/*
+ * Read packing over a page bitmap: walk pages in ascending address order; a
+ * run starts at a set page whose predecessor is unset, or when the current run
+ * already has max_run pages; it extends while the next page is set.
+ * runs[2j] = start, runs[2j+1] = length.  Returns the number of runs in *n_runs.
+ */
+int jo_runs(const uint32_t *bitmap, int num_phys_pages, int max_run,
+            int32_t *runs, int32_t *n_runs)
+{
+    if (num_phys_pages < 0 || max_run < 1)
+        return -1;
+    int n = 0;
+    int p = 0;
+    while (p < num_phys_pages) {
+        if (!bit_at(bitmap, p)) {
+            p++;
+            continue;
+        }
+        int start = p;
+        int len = 0;
+        while (p < num_phys_pages && bit_at(bitmap, p) && len < max_run) {
+            len++;
+            p++;
+        }
+        runs[2 * n] = start;
+        runs[2 * n + 1] = len;
+        n++;
+    }
+    *n_runs = n;
+    return 0;
+}
+
+/*
+ * Corrective-read set (Eq. 2 and the following paragraph): miss = A minus the
+ * predicted set, per page.  counts = {|A|, |P|, |A and P|, |miss|, #miss runs}.
+ */
+int jo_predict_diff(const uint32_t *actual, const uint32_t *predicted, int num_phys_pages,
+                    int max_run, uint32_t *miss, int32_t *miss_runs, int32_t *counts)
+{
+    if (num_phys_pages < 0 || max_run < 1)
+        return -1;
+    int nwords = (num_phys_pages + 31) / 32;
+    int ca = 0, cp = 0, cap = 0, cm = 0;
+    for (int w = 0; w < nwords; w++)
+        miss[w] = 0;
+    for (int p = 0; p < num_phys_pages; p++) {
+        int a = bit_at(actual, p), q = bit_at(predicted, p);
+        ca += a;
+        cp += q;
+        cap += a && q;
+        if (a && !q) {
+            cm++;
+            miss[p / 32] |= 1u << (p % 32);
+        }
+    }
+    int32_t nr = 0;
+    jo_runs(miss, num_phys_pages, max_run, miss_runs, &nr);
+    counts[0] = ca;
+    counts[1] = cp;
+    counts[2] = cap;
+    counts[3] = cm;
+    counts[4] = nr;
+    return 0;
+}
+
+/*
+ * Sparse attention over the selected tokens of each query row.
+ * q [nrows, Hq, dqk] bf16: the queries of the given rows, in the given order;
+ * K row of session-local token s of session b:
+ *   k_pool + ((pt_b[s / page_size] * page_size) + s % page_size) * k_row_stride,
+ * its first dqk elements; V row likewise from v_pool, first dv elements (for
+ * the latent-KV layout v_pool == k_pool and V is the head of the K row).
+ * sel [nrows, k]: row r's selected ids; ids outside [0, M_b + i] are padding.
+ * out [nrows, Hq, dv]: softmax_s(scale * q.K_s) weighted sum of V_s;
+ * lse [nrows, Hq] (may be NULL): log-sum-exp of the scaled logits.
+ * A row with no valid id gives out = 0 and lse = -inf.
+ */
+int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len,
+                   int nrows, const int32_t *rows,
+                   const uint16_t *q, int Hq, int dqk, int dv,
+                   const uint16_t *k_pool, const uint16_t *v_pool,
+                   int64_t k_row_stride, int64_t v_row_stride,
+                   const int32_t *page_table, int pt_ld, int page_size,
+                   const int32_t *sel, int k, double scale,
+                   double *out, double *lse)
+{
+    if (nseq < 1 || Hq < 1 || dqk < 1 || dv < 1 || k < 1 || page_size < 1 || nrows < 0)
+        return -1;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int r = 0; r < nrows; r++) {
+        int g = rows[r];
+        if (g < 0 || g >= q_start[nseq]) {
+            bad = 1;
+            continue;
+        }
+        int b = session_of(nseq, q_start, g);
+        int64_t lim = (int64_t)hist_len[b] + (g - q_start[b]); /* last causal id */
+        double *logit = (double *)malloc(sizeof(double) * (size_t)k);
+        int64_t *krow = (int64_t *)malloc(sizeof(int64_t) * (size_t)k);
+        int64_t *vrow = (int64_t *)malloc(sizeof(int64_t) * (size_t)k);
+        int nv = 0;
+        for (int j = 0; j < k; j++) {
+            int64_t s = sel[(int64_t)r * k + j];
+            if (s < 0 || s > lim)
+                continue;
+            int64_t lp = s / page_size;
+            if (lp >= pt_ld) {
+                bad = 1;
+                continue;
+            }
+            int64_t phys = page_table[(int64_t)b * pt_ld + lp];
+            int64_t slot = phys * page_size + s % page_size;
+            krow[nv] = slot * k_row_stride;
+            vrow[nv] = slot * v_row_stride;
+            nv++;
+        }
+        for (int h = 0; h < Hq; h++) {
+            const uint16_t *qh = q + ((int64_t)r * Hq + h) * dqk;
+            double *o = out + ((int64_t)r * Hq + h) * dv;
+            for (int e = 0; e < dv; e++)
+                o[e] = 0.0;
+            if (nv == 0) {
+                if (lse)
+                    lse[(int64_t)r * Hq + h] = -INFINITY;
+                continue;
+            }
+            double m = -INFINITY;
+            for (int j = 0; j < nv; j++) {
+                double x = 0.0;
+                for (int e = 0; e < dqk; e++)
+                    x += jo_bf16_value(qh[e]) * jo_bf16_value(k_pool[krow[j] + e]);
+                logit[j] = scale * x;
+                if (logit[j] > m)
+                    m = logit[j];
+            }
+            double denom = 0.0;
+            for (int j = 0; j < nv; j++) {
+                double p = exp(logit[j] - m);
+                denom += p;
+                for (int e = 0; e < dv; e++)
+                    o[e] += p * jo_bf16_value(v_pool[vrow[j] + e]);
+            }
+            for (int e = 0; e < dv; e++)
+                o[e] /= denom;
+            if (lse)
+                lse[(int64_t)r * Hq + h] = m + log(denom);
+        }
+        free(vrow);
+        free(krow);
+        free(logit);
+    }
+    return bad ? -2 : 0;
+}
