@@ -1,0 +1,211 @@
+/*
+ * janus.h - C ABI of the MI355X (gfx950) library for the sparse-selection hot
+ * path of append prefill in top-k sparse-attention LLMs.
+ *
+ * One append prefill of a layer, for a batch of sessions, is
+ *
+ *   janus_index_scores  indexer relevance of every candidate token   (Eq. 1)
+ *   janus_topk          the k best candidates per appended token     (Eq. 1)
+ *   janus_page_demand   union of the selections as a page set, plus
+ *                       address-ordered runs of adjacent pages       (union after Eq. 1;
+ *                                                                     Sec. 4.3 read packing)
+ *   janus_predict_diff  corrective-read set: actual minus predicted  (Eq. 2 and after)
+ *   janus_sparse_attn   attention over the selected tokens only      (after Eq. 1)
+ *
+ * Running index_scores + topk + page_demand on a predicted indexer query
+ * (an earlier layer's hidden state through this layer's indexer) gives the
+ * predicted union of Eq. (2).
+ *
+ * Conventions shared by every call
+ *   - Pointers named "device" are HIP device pointers the caller allocated;
+ *     the library never allocates, frees or keeps a pointer after returning.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream).
+ *     Every call only enqueues work on it and returns; no call synchronises.
+ *   - Outputs are overwritten in full (bitmaps are cleared by the call).
+ *   - Host-detectable argument errors return a status and enqueue nothing:
+ *     JANUS_ERR_INVALID_ARG for NULL required pointers and out-of-range sizes,
+ *     JANUS_ERR_UNSUPPORTED for shapes/dtypes with no kernel,
+ *     JANUS_ERR_WORKSPACE for a workspace smaller than required.
+ *     A failed launch returns JANUS_ERR_DEVICE; device faults surface at the
+ *     caller's next synchronisation.
+ *   - Workspace: when a call takes (workspace, workspace_bytes), passing
+ *     workspace == NULL stores the required byte count in *workspace_bytes and
+ *     returns JANUS_OK without enqueuing anything.  The workspace needs no
+ *     initialisation.  Calls that share a workspace must not overlap.
+ *   - Token ids are session-local: ids 0..M_b-1 are the cached history and
+ *     M_b..M_b+N_b-1 the appended tokens.  In id arrays, values outside
+ *     [0, M_b+N_b) are padding, like -1.
+ *   - Page tables map a session's logical page (id / page_size) to a physical
+ *     page of one shared pool; entries must lie in [0, num_phys_pages).
+ *   - The library is stateless and reentrant.
+ */
+#ifndef JANUS_H
+#define JANUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    JANUS_OK = 0,
+    JANUS_ERR_INVALID_ARG = 1,
+    JANUS_ERR_UNSUPPORTED = 2,
+    JANUS_ERR_WORKSPACE = 3,
+    JANUS_ERR_DEVICE = 4
+} janus_status;
+
+typedef enum {
+    JANUS_F32 = 0,
+    JANUS_BF16 = 1,
+    JANUS_FP8_E4M3 = 2 /* OCP e4m3fn: bias 7, max 448, no infinities */
+} janus_dtype;
+
+/*
+ * A ragged batch of B sessions (B = 1 for a single append prefill).  Session b
+ * has a cached history of M_b tokens and appends N_b tokens (the P and L of
+ * the paper's notation table).  Host fields size grids; device arrays locate
+ * rows.  All device arrays are int32 except score_start.
+ */
+typedef struct {
+    int32_t num_seqs;            /* B >= 1                                        */
+    int32_t total_q;             /* host: sum_b N_b                               */
+    int32_t max_q;               /* host: max_b N_b                               */
+    int32_t max_ctx;             /* host: max_b (M_b + N_b)                       */
+    int64_t total_ctx;           /* host: sum_b (M_b + N_b)                       */
+    const int32_t *q_start;      /* device [B+1]: prefix sums of N_b -> rows of
+                                    q, w, topk_idx and attention q/out            */
+    const int32_t *ctx_start;    /* device [B+1]: prefix sums of M_b+N_b -> rows
+                                    of the indexer keys and their scales          */
+    const int32_t *hist_len;     /* device [B]: M_b                               */
+    const int64_t *score_start;  /* device [B+1]: prefix sums of N_b*(M_b+N_b)    */
+} janus_batch;
+
+/*
+ * Indexer scores (Eq. 1; the indexer form is the multi-head ReLU-weighted
+ * dot product of the lightning indexer, which the paper leaves to the
+ * model's report).  For appended token i of session b (absolute position
+ * M_b+i) and candidate s in [0, M_b+i]:
+ *
+ *   S[i,s] = q_scale[i] * k_scale[s] * sum_{h<H} w[i,h] * max(0, sum_{j<d} q[i,h,j] * kI[s,j])
+ *
+ * Candidates s > M_b+i (later appended tokens) are written as -inf.
+ *   q       device [total_q, H, d], dtype q_dt (row-major)
+ *   q_scale device [total_q] fp32 (> 0), or NULL for 1
+ *   kI      device [total_ctx, d], dtype k_dt; session b's keys start at row
+ *           ctx_start[b] (history first, then the appended tokens)
+ *   k_scale device [total_ctx] fp32 (> 0), or NULL for 1
+ *   w       device [total_q, H] fp32, w >= 0
+ *   scores  device fp32; row i of session b starts at
+ *           scores + score_start[b] + i*(M_b+N_b) and holds M_b+N_b entries.
+ * q_dt must equal k_dt.  fp8 and bf16 with d = 128 and H a multiple of 16 run
+ * on MFMA; other shapes and fp32 run on a plain vector kernel.
+ * Accumulation is fp32.
+ */
+int janus_index_scores(const janus_batch *b,
+                       const void *q, janus_dtype q_dt, const float *q_scale,
+                       const void *kI, janus_dtype k_dt, const float *k_scale,
+                       const float *w, int H, int d,
+                       float *scores, void *stream);
+
+/*
+ * Top-k per appended token (the selection of Eq. 1): the k largest scores of
+ * row i over candidates [0, M_b+i] under the strict order (score descending,
+ * id ascending), so ties go to the lower id and -0.0 equals +0.0.  Rows with
+ * fewer than k candidates select all of them.
+ *   scores    device, laid out as written by janus_index_scores
+ *   topk_idx  device [total_q, k] int32: the selected ids in ascending id
+ *             order, then -1 padding.
+ * Requires 1 <= k <= 6144 (rows with at most k candidates have no limit).
+ * No workspace is needed: pass workspace = NULL with *workspace_bytes set to
+ * anything, or query it (always 0).
+ */
+int janus_topk(const janus_batch *b, const float *scores, int k,
+               int32_t *topk_idx, void *workspace, size_t *workspace_bytes,
+               void *stream);
+
+/*
+ * Page demand (the union of the per-token selections that must be loaded
+ * before attention, mapped to pages) and read packing (Sec. 4.3: one read per
+ * maximal run of selected, physically adjacent pages; never an unselected
+ * page), with runs split from their low end into pieces of at most max_run.
+ *
+ *   A = { page_table[b, s / page_size] : s in topk_idx rows of session b,
+ *                                        0 <= s < min(limit_b, M_b+N_b) }
+ *
+ *   topk_idx   device [total_q, k] int32 session-local ids (others: padding)
+ *   page_table device [B, pt_ld] int32
+ *   page_size  power of two >= 1
+ *   limit      device [B] int32, or NULL for M_b (history pages only: the
+ *              appended tokens' KV is produced in HBM and never loaded)
+ *   bitmap     device [ceil(num_phys_pages/32)] uint32; page p is bit p%32 of
+ *              word p/32
+ *   page_list  device [num_phys_pages] int32: the set pages, ascending
+ *   runs       device [2*num_phys_pages] int32: (start, length) pairs,
+ *              ascending by start
+ *   counts     device [2] int32: {number of pages, number of runs}
+ * Requires num_phys_pages <= 2^24 and max_run >= 1.
+ */
+int janus_page_demand(const janus_batch *b, const int32_t *topk_idx, int k,
+                      const int32_t *page_table, int pt_ld, int page_size,
+                      const int32_t *limit, int num_phys_pages, int max_run,
+                      uint32_t *bitmap, int32_t *page_list, int32_t *runs,
+                      int32_t *counts, void *workspace, size_t *workspace_bytes,
+                      void *stream);
+
+/*
+ * Corrective reads (Eq. 2 and the paragraph after it): pages of the actual
+ * set A absent from the predicted set P, as a bitmap and as packed runs, with
+ * the counts behind recall |A&P|/|A| and precision |A&P|/|P|.
+ *   actual, predicted  device [ceil(num_phys_pages/32)] uint32 bitmaps
+ *   miss               device [ceil(num_phys_pages/32)] uint32: A & ~P
+ *   miss_runs          device [2*num_phys_pages] int32 (start, length) pairs
+ *   counts             device [5] int32: {|A|, |P|, |A&P|, |A&~P|, #miss runs}
+ * Requires num_phys_pages <= 2^24 and max_run >= 1.
+ */
+int janus_predict_diff(const uint32_t *actual, const uint32_t *predicted,
+                       int num_phys_pages, int max_run,
+                       uint32_t *miss, int32_t *miss_runs, int32_t *counts,
+                       void *stream);
+
+/*
+ * Sparse attention over the selected tokens (the KV of S_t feeds core
+ * attention; the paragraph after Eq. 1).  All Hq query heads share one KV
+ * head (MQA; MLA in its absorbed form is the case dqk = 576, dv = 512 with V
+ * the first 512 elements of each cached 576-element latent+rope row).
+ *
+ *   out[i,h,:] = sum_{s in S_i} p_s V_s,  p = softmax_s(scale * q[i,h,:] . K_s)
+ *   lse[i,h]   = log sum_{s in S_i} exp(scale * q[i,h,:] . K_s)
+ *
+ * S_i = the ids of row i of topk_idx that lie in [0, M_b+i] (others are
+ * padding).  K_s is the first dqk elements of pool row
+ * (page_table[b, s/page_size]*page_size + s%page_size) of k_pool, V_s the
+ * first dv elements of the same row of v_pool.
+ *   q       device [total_q, Hq, dqk] bf16
+ *   k_pool  device bf16 rows of k_row_stride elements (>= dqk)
+ *   v_pool  device bf16 rows of v_row_stride elements (>= dv); may equal k_pool
+ *   out     device [total_q, Hq, dv], out_dt JANUS_BF16 or JANUS_F32
+ *   lse     device [total_q, Hq] fp32, or NULL
+ * A row with no valid id gets out = 0 and lse = -inf.  Softmax and
+ * accumulation are fp32; products run on bf16 MFMA for Hq a multiple of 32,
+ * dqk = 576, dv = 512 and v_pool == k_pool, else on a plain vector kernel.
+ */
+int janus_sparse_attn(const janus_batch *b,
+                      const void *q, int Hq, int dqk, int dv,
+                      const void *k_pool, const void *v_pool,
+                      int64_t k_row_stride, int64_t v_row_stride,
+                      const int32_t *page_table, int pt_ld, int page_size,
+                      const int32_t *topk_idx, int k, float scale,
+                      void *out, janus_dtype out_dt, float *lse,
+                      void *stream);
+
+/* Static description of a status code. */
+const char *janus_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JANUS_H */

@@ -1,0 +1,108 @@
+"""The C ABI library loads, exports every declared entry point, and rejects bad
+arguments on the host (these calls return before touching a device)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "janus.h")
+LIB = os.path.join(ROOT, "paper_2609_36938_amd", "libjanus.so")
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced on the host
+
+
+def _ensure_lib():
+    if not os.path.exists(LIB):
+        from paper_2609_36938_amd import build
+        build.build()
+    return LIB
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(janus_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_five_calls():
+    syms = declared_symbols()
+    for s in ("janus_index_scores", "janus_topk", "janus_page_demand", "janus_predict_diff",
+              "janus_sparse_attn", "janus_status_string"):
+        assert s in syms
+
+
+def test_library_exports_every_declared_symbol():
+    out = subprocess.check_output(["nm", "-D", "--defined-only", _ensure_lib()], text=True)
+    exported = set(l.split()[-1] for l in out.splitlines() if " T " in l)
+    missing = [s for s in declared_symbols() if s not in exported]
+    assert not missing, missing
+    L = ctypes.CDLL(LIB)
+    for s in declared_symbols():
+        assert hasattr(L, s)
+
+
+def test_header_compiles_as_c():
+    r = subprocess.run(["gcc", "-std=c99", "-Wall", "-Werror", "-fsyntax-only", "-x", "c", HEADER],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+
+
+@pytest.fixture(scope="module")
+def L():
+    import paper_2609_36938_amd as janus
+    _ensure_lib()
+    return janus.lib()
+
+
+def _batch(total_q=4, max_ctx=100, B=1):
+    import paper_2609_36938_amd as janus
+    return janus._Batch(B, total_q, total_q, max_ctx, max_ctx, FAKE.value, FAKE.value, FAKE.value, FAKE.value)
+
+
+def test_status_strings(L):
+    assert L.janus_status_string(0) == b"ok"
+    assert L.janus_status_string(1) == b"invalid argument"
+    assert L.janus_status_string(2) == b"unsupported shape or dtype"
+    assert L.janus_status_string(99) == b"unknown status"
+
+
+def test_invalid_arguments_are_rejected_on_host(L):
+    b = _batch()
+    ws = ctypes.c_size_t(123)
+    # NULL batch / pointers
+    assert L.janus_topk(None, FAKE, 8, FAKE, None, ctypes.byref(ws), None) == 1
+    assert L.janus_topk(ctypes.byref(b), None, 8, FAKE, None, ctypes.byref(ws), None) == 1
+    assert L.janus_topk(ctypes.byref(b), FAKE, 0, FAKE, None, ctypes.byref(ws), None) == 1
+    assert ws.value == 0  # top-k needs no workspace
+    # k above the supported maximum
+    assert L.janus_topk(ctypes.byref(b), FAKE, 7000, FAKE, None, ctypes.byref(ws), None) == 2
+    # mismatched indexer dtypes, bad dtype code, bad sizes
+    assert L.janus_index_scores(ctypes.byref(b), FAKE, 2, None, FAKE, 1, None, FAKE, 64, 128, FAKE, None) == 2
+    assert L.janus_index_scores(ctypes.byref(b), FAKE, 7, None, FAKE, 7, None, FAKE, 64, 128, FAKE, None) == 1
+    assert L.janus_index_scores(ctypes.byref(b), FAKE, 2, None, FAKE, 2, None, FAKE, 0, 128, FAKE, None) == 1
+    # page size must be a power of two; max_run >= 1
+    args = [ctypes.byref(b), FAKE, 8, FAKE, 4, 48, None, 100, 32, FAKE, FAKE, FAKE, FAKE, None,
+            ctypes.byref(ws), None]
+    assert L.janus_page_demand(*args) == 1
+    args[5], args[8] = 64, 0
+    assert L.janus_page_demand(*args) == 1
+    args[8], args[7] = 32, (1 << 19) + 1
+    assert L.janus_page_demand(*args) == 2
+    assert L.janus_predict_diff(FAKE, None, 10, 32, FAKE, FAKE, FAKE, None) == 1
+    assert L.janus_predict_diff(FAKE, FAKE, 10, 0, FAKE, FAKE, FAKE, None) == 1
+    # attention: output dtype, row strides shorter than the head dims
+    assert L.janus_sparse_attn(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 576, 576, FAKE, 4, 64, FAKE,
+                               8, ctypes.c_float(0.1), FAKE, 2, None, None) == 2
+    assert L.janus_sparse_attn(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 500, 576, FAKE, 4, 64, FAKE,
+                               8, ctypes.c_float(0.1), FAKE, 1, None, None) == 1
+
+
+def test_product_path_does_not_touch_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2609_36938_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in text and "janus_oracle" not in text, f
