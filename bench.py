@@ -1,0 +1,207 @@
+"""Benchmark: one layer's append-prefill hot path on one MI355X.
+
+Workload: history M = 131072 tokens + N = 8192 appended tokens, lightning
+indexer 64 heads x 128 dims in fp8 e4m3fn with per-token scales, k = 2048,
+64-token pages behind a seeded random page table, sparse MLA attention with
+128 query heads over 576-dim bf16 latent+rope rows (V = first 512 dims).
+
+A step is the whole path for the layer on one stream:
+    janus_index_scores -> janus_topk -> janus_page_demand (bitmap, list, runs)
+    -> janus_predict_diff (against the predicted set of this layer, produced
+       before the timed region by the same three calls on the predicted
+       query, as a lookahead run at an earlier layer would have)
+    -> janus_sparse_attn.
+value = appended tokens per second per layer (N * steps / time).
+
+Printed as one JSON line (see the keys below), with the roofline of the
+dominant kernel (index scores, fp8 MFMA) from HIP events on the launch stream,
+and the CPU oracle timed on a bounded row sample on the host cores.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP8 = 5.0e15      # dense fp8 MFMA, FLOP/s
+PEAK_BF16 = 2.5e15     # dense bf16 MFMA, FLOP/s
+PEAK_HBM = 8.0e12      # bytes/s
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=64, help="query rows in the oracle's timed sample")
+    p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "index_scores_traffic.json"))
+    return p.parse_args()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path (see DESIGN.md, sharding).",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2609_36938_amd as janus
+    from workloads import attention_inputs, config
+
+    t_gen = time.time()
+    wl = config(2, with_pred=True)
+    ai = attention_inputs(wl)
+    t_gen = time.time() - t_gen
+    dev = torch.device("cuda:0")
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    bt = janus.Batch(wl.hist_len, wl.new_len, device=dev)
+    q, kI, w, sq, sk = T(wl.q), T(wl.kI), T(wl.w), T(wl.q_scale), T(wl.k_scale)
+    qp, sqp = T(wl.q_pred), T(wl.q_pred_scale)
+    pt = T(wl.page_table)
+    qa = T(ai.q)
+    kv = T(ai.k_pool)
+    P, ps, k, mr = wl.num_phys_pages, wl.page_size, wl.k, wl.max_run
+    N, M = wl.total_q, int(wl.hist_len[0])
+
+    scores = torch.empty(bt.total_scores, dtype=torch.float32, device=dev)
+    sel = torch.empty((N, k), dtype=torch.int32, device=dev)
+    nw = (P + 31) // 32
+    pd_out = (torch.empty(nw, dtype=torch.int32, device=dev), torch.empty(P, dtype=torch.int32, device=dev),
+              torch.empty(2 * P, dtype=torch.int32, device=dev), torch.empty(2, dtype=torch.int32, device=dev))
+    diff_out = (torch.empty(nw, dtype=torch.int32, device=dev), torch.empty(2 * P, dtype=torch.int32, device=dev),
+                torch.empty(5, dtype=torch.int32, device=dev))
+    out = torch.empty((N, ai.Hq, ai.dv), dtype=torch.bfloat16, device=dev)
+    lse = torch.empty((N, ai.Hq), dtype=torch.float32, device=dev)
+
+    # predicted set of this layer (lookahead run, outside the timed region)
+    janus.index_scores(bt, qp, kI, w, q_scale=sqp, k_scale=sk, scores=scores)
+    sel_p = janus.topk(bt, scores, k)
+    pred_bm = janus.page_demand(bt, sel_p, pt, ps, P, mr)[0].clone()
+    torch.cuda.synchronize()
+
+    names = ["index_scores", "topk", "page_demand", "predict_diff", "sparse_attn"]
+
+    def step(ev=None):
+        if ev:
+            ev[0].record()
+        janus.index_scores(bt, q, kI, w, q_scale=sq, k_scale=sk, scores=scores)
+        if ev:
+            ev[1].record()
+        janus.topk(bt, scores, k, out=sel)
+        if ev:
+            ev[2].record()
+        janus.page_demand(bt, sel, pt, ps, P, mr, out=pd_out)
+        if ev:
+            ev[3].record()
+        janus.predict_diff(pd_out[0], pred_bm, P, mr, out=diff_out)
+        if ev:
+            ev[4].record()
+        janus.sparse_attn(bt, qa, kv, kv, pt, ps, sel, ai.scale, dv=ai.dv, out=out, lse=lse)
+        if ev:
+            ev[5].record()
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"# inputs generated in {t_gen:.1f}s; warmup done", file=sys.stderr, flush=True)
+
+    # timed region: K steps, bracketed by synchronisation
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    # per-kernel durations: HIP events on the launch stream, separate pass
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    for e in evs:
+        step(e)
+    torch.cuda.synchronize()
+    per = {n: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, n in enumerate(names)}
+
+    # algorithmic work
+    pairs = N * (M + 1) + N * (N - 1) // 2                  # causal (token, candidate) pairs
+    idx_flop = 2.0 * wl.H * wl.d * pairs
+    topk_bytes = 4.0 * pairs + 4.0 * N * k
+    attn_rows = N * k                                         # every row of this workload selects k ids
+    gather_bytes = attn_rows * ai.dqk * 2.0
+    attn_flop = 2.0 * N * ai.Hq * k * (ai.dqk + ai.dv)
+    t_idx = per["index_scores"] * 1e-3
+    ach = idx_flop / t_idx
+    traffic = None
+    if os.path.exists(args.traffic):
+        try:
+            tr = json.load(open(args.traffic))
+            traffic = tr.get("bytes_per_launch")
+        except Exception:
+            traffic = None
+
+    ms_step = wall / args.steps * 1e3
+    counts = diff_out[2].cpu().tolist()
+    rec = {
+        "metric": "new tokens/s per layer (indexer+top-k+sparse attn) at 128K history; % MFMA/HBM peak",
+        "value": N * args.steps / wall,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8+bf16",
+        "data": "synthetic",
+        "config": {"workload": "DeepSeek-V3.2-shaped layer, history 131072 + 8192 new tokens, k=2048, "
+                               "64-token pages behind a random page table",
+                   "history": M, "new_tokens": N, "indexer": "64 heads x 128 fp8 e4m3fn, per-token scales",
+                   "k": k, "page_size": ps, "attention": "MLA-MQA 128 heads, 576/512 bf16"},
+        "roofline": {"bound": "mfma", "kernel": "index_scores", "achieved": ach / 1e12, "peak": PEAK_FP8 / 1e12,
+                     "unit": "TFLOP/s", "frac": ach / PEAK_FP8, "traffic": traffic},
+        "kernels_ms": per,
+        "kernel_rates": {
+            "index_scores_TFLOPs": idx_flop / t_idx / 1e12,
+            "topk_GBps": topk_bytes / (per["topk"] * 1e-3) / 1e9,
+            "topk_frac_hbm": topk_bytes / (per["topk"] * 1e-3) / PEAK_HBM,
+            "sparse_attn_gather_GBps_logical": gather_bytes / (per["sparse_attn"] * 1e-3) / 1e9,
+            "sparse_attn_gather_frac_hbm": gather_bytes / (per["sparse_attn"] * 1e-3) / PEAK_HBM,
+            "sparse_attn_TFLOPs": attn_flop / (per["sparse_attn"] * 1e-3) / 1e12,
+            "sparse_attn_frac_bf16_mfma": attn_flop / (per["sparse_attn"] * 1e-3) / PEAK_BF16,
+        },
+        "demand": {"pages": int(pd_out[3][0]), "runs": int(pd_out[3][1]), "pred_counts": counts},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows)
+    print(json.dumps(rec))
+
+
+def cpu_baseline(wl, ai, nrows):
+    """The oracle, untuned, on a stride sample of query rows: scores, top-k and
+    attention for each sampled row (page demand is negligible beside them)."""
+    import oracle
+    from workloads import attention_q_rows
+
+    rows = np.linspace(0, wl.total_q - 1, nrows).astype(np.int32)
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    t0 = time.perf_counter()
+    sc = oracle.index_scores(wl.q_start, wl.hist_len, wl.q, "fp8", wl.q_scale, wl.kI, "fp8", wl.k_scale, wl.w, rows)
+    sel = oracle.topk(wl.q_start, wl.hist_len, rows, sc.astype(np.float32), wl.k)
+    qr = attention_q_rows(wl, rows)
+    oracle.sparse_attn(wl.q_start, wl.hist_len, rows, qr, ai.k_pool, None, ai.k_row_stride, ai.v_row_stride,
+                       wl.page_table, wl.page_size, sel, ai.scale, ai.dv)
+    dt = time.perf_counter() - t0
+    return {"value": nrows / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{nrows} evenly spaced query rows of the same workload (scores over all "
+                      f"~139K candidates, top-k, attention over k=2048); {dt:.1f} s"}
+
+
+if __name__ == "__main__":
+    main()
