@@ -43,6 +43,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-rows", type=int, default=64, help="query rows in the oracle's timed sample")
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "index_scores_traffic.json"))
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run a plain 1 GiB device copy (known bytes) for HBM counter calibration")
     return p.parse_args()
 
 
@@ -112,6 +114,12 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.copy_calibration:
+        src = torch.empty(1 << 28, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)  # reads 1 GiB, writes 1 GiB
+        torch.cuda.synchronize()
+        del src, dst
     print(f"# inputs generated in {t_gen:.1f}s; warmup done", file=sys.stderr, flush=True)
 
     # timed region: K steps, bracketed by synchronisation

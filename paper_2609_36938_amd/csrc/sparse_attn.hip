@@ -19,29 +19,45 @@ namespace janus {
 constexpr int MLA_DQK = 576;
 constexpr int MLA_DV = 512;
 constexpr int MLA_KT = 32;                  // keys per tile
-constexpr int MLA_KP = MLA_DQK + 8;         // K tile pitch (elements): 1168 B staggers the banks
-constexpr int MLA_VTP = MLA_KT / 2 + 4;     // V^T pitch in dwords (key pairs): 80 B
 constexpr int MLA_STEPS = MLA_DQK / 32;     // MFMA K-steps over the 576 dims
 constexpr int MLA_NB = MLA_DV / 16;         // 16-wide dv blocks
 constexpr float LOG2E = 1.4426950408889634f;
 constexpr float LN2 = 0.6931471805599453f;
 
 JANUS_DEV v8bf as_v8bf(v4i x) { return __builtin_bit_cast(v8bf, x); }
+typedef short v8s16 __attribute__((ext_vector_type(8)));
 
-template <int NW, int HB>
-__global__ __launch_bounds__(64 * NW, (NW >= 8 ? 2 : 1)) void sparse_mla_mfma(
+constexpr int MLA_CPR = MLA_DQK * 2 / 16;      // 16-byte chunks per cached row (72)
+constexpr int MLA_PCH = MLA_CPR + 1;            // LDS row pitch in chunks: 1168 B, 16 rows -> 16 bank groups
+constexpr int MLA_ROWB = MLA_PCH * 16;          // LDS bytes per tile row
+constexpr int MLA_TILE_CH = MLA_KT * MLA_PCH;   // chunks per tile (2336)
+constexpr int MLA_TILE_INS = (MLA_TILE_CH + 63) / 64;  // wave-instructions per tile (37)
+constexpr int MLA_MAX_K = 4096;                 // selected ids per token held in LDS
+constexpr float RESCALE_SLACK = 8.0f;           // log2 headroom before O is rescaled
+
+typedef short v4s16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) v4s16 lds_v4s16;
+
+// Transposing LDS read (ds_read_b64_tr_b16): within each 16-lane group,
+// lane i's element j is element i%4 of the 8 bytes addressed by lane 4j+i/4.
+JANUS_DEV v4s16 lds_read_tr16(const uint8_t *lds_base, int byte_off)
+{
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (lds_v4s16 *)((__attribute__((address_space(3))) uint8_t *)lds_base + byte_off));
+}
+
+template <int NW>
+__global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ kv, int64_t row_stride,
     const int32_t *__restrict__ page_table, int pt_ld, int page_shift, const int32_t *__restrict__ topk,
     int k, float scale_log2, void *__restrict__ out, int out_f32, float *__restrict__ lse)
 {
-    constexpr int HQ = 16 * HB * NW;
-    constexpr int HW = 16 * HB;  // heads per wave
+    constexpr int HQ = 16 * NW;  // one 16-head MFMA block per wave
     constexpr int NT = 64 * NW;
-    __shared__ __attribute__((aligned(16))) uint16_t sK[MLA_KT * MLA_KP];
-    __shared__ __attribute__((aligned(16))) uint32_t sVt[MLA_DV * MLA_VTP];
-    __shared__ int64_t sSlot[MLA_KT];
-    __shared__ int sAny;
+    __shared__ __attribute__((aligned(16))) uint8_t sKV[2][MLA_TILE_INS * 64 * 16];
+    __shared__ int32_t sSlot[MLA_MAX_K];
 
     const int g = blockIdx.x;
     const int b = session_of_row(q_start, num_seqs, g);
@@ -50,116 +66,91 @@ __global__ __launch_bounds__(64 * NW, (NW >= 8 ? 2 : 1)) void sparse_mla_mfma(
     const int psz_mask = (1 << page_shift) - 1;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int c16 = lane & 15, grp = lane >> 4;
+    const int head0 = 16 * wave;
 
-    // queries of heads HW*wave + 16*hb + c16, dims 32*step + 8*grp .. +7
-    v8bf qf[HB][MLA_STEPS];
-#pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        const uint16_t *qr = q + ((int64_t)g * HQ + HW * wave + 16 * hb + c16) * MLA_DQK + 8 * grp;
+    // physical row of every selected id (-1: padding)
+    for (int j = tid; j < k; j += NT) {
+        const int s = topk[(int64_t)g * k + j];
+        sSlot[j] = (s >= 0 && s <= lim) ? ((pt[s >> page_shift] << page_shift) + (s & psz_mask)) : -1;
+    }
+    // queries of head head0 + c16, dims 32*step + 8*grp .. +7
+    v8bf qf[MLA_STEPS];
+    {
+        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + c16) * MLA_DQK + 8 * grp;
 #pragma unroll
         for (int st = 0; st < MLA_STEPS; ++st)
-            qf[hb][st] = as_v8bf(*(const v4i *)(qr + 32 * st));
+            qf[st] = as_v8bf(*(const v4i *)(qr + 32 * st));
     }
-    v4f o[HB][MLA_NB];
+    v4f o[MLA_NB];
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb)
-#pragma unroll
-        for (int nb = 0; nb < MLA_NB; ++nb)
-            o[hb][nb] = v4f{0.f, 0.f, 0.f, 0.f};
-    float m[HB], lsum[HB];
-#pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        m[hb] = -INFINITY;
-        lsum[hb] = 0.f;
-    }
+    for (int nb = 0; nb < MLA_NB; ++nb)
+        o[nb] = v4f{0.f, 0.f, 0.f, 0.f};
+    float m = -INFINITY, lsum = 0.f;  // per head head0 + c16
+    __syncthreads();
 
-    for (int t0 = 0; t0 < k; t0 += MLA_KT) {
-        if (tid == 0)
-            sAny = 0;
-        __syncthreads();
-        if (tid < MLA_KT) {
-            int64_t slot = -1;
-            if (t0 + tid < k) {
-                const int s = topk[(int64_t)g * k + t0 + tid];
-                if (s >= 0 && s <= lim)
-                    slot = ((int64_t)pt[s >> page_shift] << page_shift) + (s & psz_mask);
+    const int ntiles = (k + MLA_KT - 1) / MLA_KT;
+    // gather of tile t into buffer: wave-instruction j fills LDS chunks 64j .. 64j+63
+    // (chunk 72 of each row is padding and loads a dummy; padding ids load row 0)
+    auto issue = [&](int t, int buf) {
+        for (int j = wave; j < MLA_TILE_INS; j += NW) {
+            const int qch = 64 * j + lane;
+            if (qch < MLA_TILE_CH) {
+                const int r = qch / MLA_PCH;
+                int c = qch - r * MLA_PCH;
+                if (c == MLA_CPR)
+                    c = 0;
+                const int key = MLA_KT * t + r;
+                int slot = key < k ? sSlot[key] : -1;
+                if (slot < 0)
+                    slot = 0;  // padding rows read a real row; their logits are masked
+                const uint16_t *src = kv + (int64_t)slot * row_stride + 8 * c;
+                __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(&sKV[buf][(64 * j) * 16]), 16,
+                                                 0, 0);
             }
-            sSlot[tid] = slot;
-            if (slot >= 0)
-                sAny = 1;
         }
-        __syncthreads();
-        if (!sAny)
-            continue;
-        // gather: (key pair p, 16-byte chunk c) items
-        for (int item = tid; item < (MLA_KT / 2) * (MLA_DQK / 8); item += NT) {
-            const int p = item / (MLA_DQK / 8), c = item % (MLA_DQK / 8);
-            const int64_t s0 = sSlot[2 * p], s1 = sSlot[2 * p + 1];
-            v4i r0 = v4i{0, 0, 0, 0}, r1 = v4i{0, 0, 0, 0};
-            if (s0 >= 0)
-                r0 = *(const v4i *)(kv + s0 * row_stride + 8 * c);
-            if (s1 >= 0)
-                r1 = *(const v4i *)(kv + s1 * row_stride + 8 * c);
-            *(v4i *)&sK[(2 * p) * MLA_KP + 8 * c] = r0;
-            *(v4i *)&sK[(2 * p + 1) * MLA_KP + 8 * c] = r1;
-            if (c < MLA_DV / 8) {
+    };
+    issue(0, 0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+
+    for (int t = 0; t < ntiles; ++t) {
+        const int buf = t & 1;
+        if (t + 1 < ntiles)
+            issue(t + 1, buf ^ 1);
+        const uint8_t *tile = sKV[buf];
+        // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
+        v4f st[2];
 #pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const uint32_t a = (uint32_t)r0[e], bb = (uint32_t)r1[e];
-                    sVt[(8 * c + 2 * e) * MLA_VTP + p] = (a & 0xffffu) | (bb << 16);
-                    sVt[(8 * c + 2 * e + 1) * MLA_VTP + p] = (a >> 16) | (bb & 0xffff0000u);
-                }
+        for (int kb = 0; kb < 2; ++kb) {
+            st[kb] = v4f{0.f, 0.f, 0.f, 0.f};
+            const int r = 16 * kb + c16;
+            const uint8_t *row = tile + r * MLA_ROWB;
+#pragma unroll
+            for (int step = 0; step < MLA_STEPS; ++step) {
+                const v8bf a = as_v8bf(*(const v4i *)(row + 16 * (4 * step + grp)));
+                st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[step], st[kb], 0, 0, 0);
             }
         }
-        __syncthreads();
-        // S^T[key][head] = K Q^T: 2 key blocks x HB head blocks
-        v4f st[2][HB];
+        // online softmax (exp2 domain) with lazy rescaling of O
+        float x[2][4];
+        float mx = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int hb = 0; hb < HB; ++hb)
-                st[kb][hb] = v4f{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int step = 0; step < MLA_STEPS; ++step) {
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                const v8bf a = as_v8bf(*(const v4i *)&sK[(16 * kb + c16) * MLA_KP + 32 * step + 8 * grp]);
-#pragma unroll
-                for (int hb = 0; hb < HB; ++hb)
-                    st[kb][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[hb][step], st[kb][hb], 0, 0, 0);
+            for (int i = 0; i < 4; ++i) {
+                const int key = MLA_KT * t + 16 * kb + 4 * grp + i;
+                const bool ok = key < k && sSlot[key] >= 0;
+                x[kb][i] = ok ? st[kb][i] * scale_log2 : -INFINITY;
+                mx = fmaxf(mx, x[kb][i]);
             }
-        }
-        // online softmax per head (column c16 of each head block)
-        v8bf pa[HB];
-#pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-            float x[2][4];
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const bool ok = sSlot[16 * kb + 4 * grp + i] >= 0;
-                    x[kb][i] = ok ? st[kb][hb][i] * scale_log2 : -INFINITY;
-                    mx = fmaxf(mx, x[kb][i]);
-                }
-            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const float mnew = fmaxf(m[hb], mx);
-            const bool none = mnew == -INFINITY;
-            const float alpha = none ? 1.f : exp2f(m[hb] - mnew);
-            float ps = 0.f;
-            float pv[2][4];
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    pv[kb][i] = none ? 0.f : exp2f(x[kb][i] - mnew);
-                    ps += pv[kb][i];
-                }
-            lsum[hb] = lsum[hb] * alpha + ps;
-            m[hb] = mnew;
-            // O rows of this lane are heads 4*grp + i of the block: fetch their alpha
+        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+        const bool grow = mx > m + RESCALE_SLACK || (m == -INFINITY && mx > -INFINITY);
+        if (__ballot(grow)) {
+            const float mnew = grow ? mx : m;
+            const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mnew);
+            lsum *= alpha;
+            m = mnew;
             float ai[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i)
@@ -168,50 +159,54 @@ __global__ __launch_bounds__(64 * NW, (NW >= 8 ? 2 : 1)) void sparse_mla_mfma(
             for (int nb = 0; nb < MLA_NB; ++nb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    o[hb][nb][i] *= ai[i];
-            pa[hb] = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
-                          (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
+                    o[nb][i] *= ai[i];
         }
-        // O += P V: K-slots of lane group grp are keys 4grp..4grp+3 and 16+4grp..16+4grp+3
+        float pv[2][4];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                pv[kb][i] = (m == -INFINITY) ? 0.f : exp2f(x[kb][i] - m);
+                lsum += pv[kb][i];
+            }
+        const v8bf pa = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
+                             (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
+        // O += P V; V operand: keys 4*grp + r' (slots 0-3) and 16 + 4*grp + r' (slots 4-7),
+        // lane (r' = c16/4, cc = c16%4) addresses dims 16*nb + 4*cc .. +3 of its key row
+        const int rr0 = 4 * grp + (c16 >> 2), rr1 = 16 + rr0, cc = c16 & 3;
+        const uint8_t *row0 = tile + rr0 * MLA_ROWB, *row1 = tile + rr1 * MLA_ROWB;
 #pragma unroll
         for (int nb = 0; nb < MLA_NB; ++nb) {
-            const uint32_t *vr = &sVt[(16 * nb + c16) * MLA_VTP];
-            v4i bv;
-            bv[0] = (int)vr[2 * grp];
-            bv[1] = (int)vr[2 * grp + 1];
-            bv[2] = (int)vr[8 + 2 * grp];
-            bv[3] = (int)vr[8 + 2 * grp + 1];
-#pragma unroll
-            for (int hb = 0; hb < HB; ++hb)
-                o[hb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[hb], as_v8bf(bv), o[hb][nb], 0, 0, 0);
+            const int ch = 2 * nb + (cc >> 1), sub = (cc & 1) * 8;
+            const v4s16 lo = lds_read_tr16(row0, 16 * ch + sub);
+            const v4s16 hi = lds_read_tr16(row1, 16 * ch + sub);
+            const v8bf bv = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+            o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, bv, o[nb], 0, 0, 0);
         }
+        __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
-    // normalise and store: O rows are heads 16*hb + 4*grp + i, column dim 16*nb + c16
+    // normalise and store: O rows are heads head0 + 4*grp + i, column dim 16*nb + c16
+    float l = lsum;
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    if (lse && grp == 0)
+        lse[(int64_t)g * HQ + head0 + c16] = l > 0.f ? (m + log2f(l)) * LN2 : -INFINITY;
+    float iv[4];
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        float l = lsum[hb];
-        l += __shfl_xor(l, 16, 64);
-        l += __shfl_xor(l, 32, 64);
-        const float inv = l > 0.f ? 1.f / l : 0.f;
-        const int head_c = HW * wave + 16 * hb + c16;
-        if (lse && grp == 0)
-            lse[(int64_t)g * HQ + head_c] = l > 0.f ? (m[hb] + log2f(l)) * LN2 : -INFINITY;
-        float iv[4];
+    for (int i = 0; i < 4; ++i)
+        iv[i] = __shfl(inv, 4 * grp + i, 64);
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
-            iv[i] = __shfl(inv, 4 * grp + i, 64);
+    for (int i = 0; i < 4; ++i) {
+        const int64_t orow = ((int64_t)g * HQ + head0 + 4 * grp + i) * MLA_DV;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int64_t orow = ((int64_t)g * HQ + HW * wave + 16 * hb + 4 * grp + i) * MLA_DV;
-#pragma unroll
-            for (int nb = 0; nb < MLA_NB; ++nb) {
-                const float v = o[hb][nb][i] * iv[i];
-                if (out_f32)
-                    ((float *)out)[orow + 16 * nb + c16] = v;
-                else
-                    ((uint16_t *)out)[orow + 16 * nb + c16] = f32_to_bf16_rne(v);
-            }
+        for (int nb = 0; nb < MLA_NB; ++nb) {
+            const float v = o[nb][i] * iv[i];
+            if (out_f32)
+                ((float *)out)[orow + 16 * nb + c16] = v;
+            else
+                ((uint16_t *)out)[orow + 16 * nb + c16] = f32_to_bf16_rne(v);
         }
     }
 }
@@ -340,7 +335,7 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
     const bool mla = dqk == MLA_DQK && dv == MLA_DV && v_pool == k_pool && v_row_stride == k_row_stride &&
                      (k_row_stride % 8) == 0 && (reinterpret_cast<uintptr_t>(k_pool) & 15) == 0 &&
                      (reinterpret_cast<uintptr_t>(q) & 15) == 0;
-    if (mla && (Hq == 128 || Hq == 64 || Hq == 32 || Hq == 16)) {
+    if (mla && k <= MLA_MAX_K && (Hq == 128 || Hq == 64 || Hq == 32 || Hq == 16)) {
         const auto *qq = (const uint16_t *)q;
         const auto *kv = (const uint16_t *)k_pool;
         auto launch = [&](auto kern, int nw) {
@@ -349,13 +344,13 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
                                of32, lse);
         };
         if (Hq == 128)
-            launch(sparse_mla_mfma<8, 1>, 8);
+            launch(sparse_mla_mfma<8>, 8);
         else if (Hq == 64)
-            launch(sparse_mla_mfma<4, 1>, 4);
+            launch(sparse_mla_mfma<4>, 4);
         else if (Hq == 32)
-            launch(sparse_mla_mfma<2, 1>, 2);
+            launch(sparse_mla_mfma<2>, 2);
         else
-            launch(sparse_mla_mfma<1, 1>, 1);
+            launch(sparse_mla_mfma<1>, 1);
         return launch_status();
     }
     if (dqk > VEC_MAX_DQK || dv > 4 * VEC_THREADS)
