@@ -14,6 +14,8 @@
 #include "janus_device.hpp"
 #include "janus_host.hpp"
 
+#include <algorithm>
+
 namespace janus {
 
 constexpr int MLA_DQK = 576;
@@ -28,7 +30,7 @@ JANUS_DEV v8bf as_v8bf(v4i x) { return __builtin_bit_cast(v8bf, x); }
 typedef short v8s16 __attribute__((ext_vector_type(8)));
 
 constexpr int MLA_CPR = MLA_DQK * 2 / 16;      // 16-byte chunks per cached row (72)
-constexpr int MLA_PCH = MLA_CPR + 1;            // LDS row pitch in chunks: 1168 B, 16 rows -> 16 bank groups
+constexpr int MLA_PCH = MLA_CPR + 2;            // LDS row pitch in chunks: 1184 B reads the K operand conflict-free
 constexpr int MLA_ROWB = MLA_PCH * 16;          // LDS bytes per tile row
 constexpr int MLA_TILE_CH = MLA_KT * MLA_PCH;   // chunks per tile (2336)
 constexpr int MLA_TILE_INS = (MLA_TILE_CH + 63) / 64;  // wave-instructions per tile (37)
@@ -47,14 +49,15 @@ JANUS_DEV v4s16 lds_read_tr16(const uint8_t *lds_base, int byte_off)
         (lds_v4s16 *)((__attribute__((address_space(3))) uint8_t *)lds_base + byte_off));
 }
 
-template <int NW>
+template <int NW, int HB>
 __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ kv, int64_t row_stride,
     const int32_t *__restrict__ page_table, int pt_ld, int page_shift, const int32_t *__restrict__ topk,
     int k, float scale_log2, void *__restrict__ out, int out_f32, float *__restrict__ lse)
 {
-    constexpr int HQ = 16 * NW;  // one 16-head MFMA block per wave
+    constexpr int HW = 16 * HB;  // heads per wave: HB 16-head MFMA blocks
+    constexpr int HQ = HW * NW;
     constexpr int NT = 64 * NW;
     __shared__ __attribute__((aligned(16))) uint8_t sKV[2][MLA_TILE_INS * 64 * 16];
     __shared__ int32_t sSlot[MLA_MAX_K];
@@ -66,38 +69,46 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int psz_mask = (1 << page_shift) - 1;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int c16 = lane & 15, grp = lane >> 4;
-    const int head0 = 16 * wave;
+    const int head0 = HW * wave;
 
     // physical row of every selected id (-1: padding)
     for (int j = tid; j < k; j += NT) {
         const int s = topk[(int64_t)g * k + j];
         sSlot[j] = (s >= 0 && s <= lim) ? ((pt[s >> page_shift] << page_shift) + (s & psz_mask)) : -1;
     }
-    // queries of head head0 + c16, dims 32*step + 8*grp .. +7
-    v8bf qf[MLA_STEPS];
-    {
-        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + c16) * MLA_DQK + 8 * grp;
+    // queries of head head0 + 16*hb + c16, dims 32*step + 8*grp .. +7
+    v8bf qf[HB][MLA_STEPS];
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb) {
+        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + 16 * hb + c16) * MLA_DQK + 8 * grp;
 #pragma unroll
         for (int st = 0; st < MLA_STEPS; ++st)
-            qf[st] = as_v8bf(*(const v4i *)(qr + 32 * st));
+            qf[hb][st] = as_v8bf(*(const v4i *)(qr + 32 * st));
     }
-    v4f o[MLA_NB];
+    v4f o[HB][MLA_NB];
 #pragma unroll
-    for (int nb = 0; nb < MLA_NB; ++nb)
-        o[nb] = v4f{0.f, 0.f, 0.f, 0.f};
-    float m = -INFINITY, lsum = 0.f;  // per head head0 + c16
+    for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+        for (int nb = 0; nb < MLA_NB; ++nb)
+            o[hb][nb] = v4f{0.f, 0.f, 0.f, 0.f};
+    float m[HB], lsum[HB];  // per head head0 + 16*hb + c16
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb) {
+        m[hb] = -INFINITY;
+        lsum[hb] = 0.f;
+    }
     __syncthreads();
 
     const int ntiles = (k + MLA_KT - 1) / MLA_KT;
     // gather of tile t into buffer: wave-instruction j fills LDS chunks 64j .. 64j+63
-    // (chunk 72 of each row is padding and loads a dummy; padding ids load row 0)
+    // (chunks 72 and 73 of each row are padding and load a dummy; padding ids load row 0)
     auto issue = [&](int t, int buf) {
         for (int j = wave; j < MLA_TILE_INS; j += NW) {
             const int qch = 64 * j + lane;
             if (qch < MLA_TILE_CH) {
                 const int r = qch / MLA_PCH;
                 int c = qch - r * MLA_PCH;
-                if (c == MLA_CPR)
+                if (c >= MLA_CPR)
                     c = 0;
                 const int key = MLA_KT * t + r;
                 int slot = key < k ? sSlot[key] : -1;
@@ -119,58 +130,72 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             issue(t + 1, buf ^ 1);
         const uint8_t *tile = sKV[buf];
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
-        v4f st[2];
+        v4f st[2][HB];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
-            st[kb] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int hb = 0; hb < HB; ++hb)
+                st[kb][hb] = v4f{0.f, 0.f, 0.f, 0.f};
             const int r = 16 * kb + c16;
             const uint8_t *row = tile + r * MLA_ROWB;
 #pragma unroll
             for (int step = 0; step < MLA_STEPS; ++step) {
                 const v8bf a = as_v8bf(*(const v4i *)(row + 16 * (4 * step + grp)));
-                st[kb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[step], st[kb], 0, 0, 0);
+#pragma unroll
+                for (int hb = 0; hb < HB; ++hb)
+                    st[kb][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[hb][step], st[kb][hb], 0, 0, 0);
             }
         }
         // online softmax (exp2 domain) with lazy rescaling of O
-        float x[2][4];
-        float mx = -INFINITY;
+        bool okk[2][4];
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const int key = MLA_KT * t + 16 * kb + 4 * grp + i;
-                const bool ok = key < k && sSlot[key] >= 0;
-                x[kb][i] = ok ? st[kb][i] * scale_log2 : -INFINITY;
-                mx = fmaxf(mx, x[kb][i]);
+                okk[kb][i] = key < k && sSlot[key] >= 0;
             }
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const bool grow = mx > m + RESCALE_SLACK || (m == -INFINITY && mx > -INFINITY);
-        if (__ballot(grow)) {
-            const float mnew = grow ? mx : m;
-            const float alpha = (m == -INFINITY) ? 0.f : exp2f(m - mnew);
-            lsum *= alpha;
-            m = mnew;
-            float ai[4];
+        v8bf pa[HB];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-                ai[i] = __shfl(alpha, 4 * grp + i, 64);
+        for (int hb = 0; hb < HB; ++hb) {
+            float x[2][4];
+            float mx = -INFINITY;
 #pragma unroll
-            for (int nb = 0; nb < MLA_NB; ++nb)
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    x[kb][i] = okk[kb][i] ? st[kb][hb][i] * scale_log2 : -INFINITY;
+                    mx = fmaxf(mx, x[kb][i]);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const bool grow = mx > m[hb] + RESCALE_SLACK || (m[hb] == -INFINITY && mx > -INFINITY);
+            if (__ballot(grow)) {
+                const float mnew = grow ? mx : m[hb];
+                const float alpha = (m[hb] == -INFINITY) ? 0.f : exp2f(m[hb] - mnew);
+                lsum[hb] *= alpha;
+                m[hb] = mnew;
+                float ai[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    o[nb][i] *= ai[i];
-        }
-        float pv[2][4];
+                    ai[i] = __shfl(alpha, 4 * grp + i, 64);
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+                for (int nb = 0; nb < MLA_NB; ++nb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                pv[kb][i] = (m == -INFINITY) ? 0.f : exp2f(x[kb][i] - m);
-                lsum += pv[kb][i];
+                    for (int i = 0; i < 4; ++i)
+                        o[hb][nb][i] *= ai[i];
             }
-        const v8bf pa = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
-                             (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
+            float pv[2][4];
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pv[kb][i] = (m[hb] == -INFINITY) ? 0.f : exp2f(x[kb][i] - m[hb]);
+                    lsum[hb] += pv[kb][i];
+                }
+            pa[hb] = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
+                          (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
+        }
         // O += P V; V operand: keys 4*grp + r' (slots 0-3) and 16 + 4*grp + r' (slots 4-7),
         // lane (r' = c16/4, cc = c16%4) addresses dims 16*nb + 4*cc .. +3 of its key row
         const int rr0 = 4 * grp + (c16 >> 2), rr1 = 16 + rr0, cc = c16 & 3;
@@ -181,32 +206,37 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             const v4s16 lo = lds_read_tr16(row0, 16 * ch + sub);
             const v4s16 hi = lds_read_tr16(row1, 16 * ch + sub);
             const v8bf bv = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
-            o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, bv, o[nb], 0, 0, 0);
+#pragma unroll
+            for (int hb = 0; hb < HB; ++hb)
+                o[hb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[hb], bv, o[hb][nb], 0, 0, 0);
         }
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
     }
-    // normalise and store: O rows are heads head0 + 4*grp + i, column dim 16*nb + c16
-    float l = lsum;
-    l += __shfl_xor(l, 16, 64);
-    l += __shfl_xor(l, 32, 64);
-    const float inv = l > 0.f ? 1.f / l : 0.f;
-    if (lse && grp == 0)
-        lse[(int64_t)g * HQ + head0 + c16] = l > 0.f ? (m + log2f(l)) * LN2 : -INFINITY;
-    float iv[4];
+    // normalise and store: O rows are heads head0 + 16*hb + 4*grp + i, column dim 16*nb + c16
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-        iv[i] = __shfl(inv, 4 * grp + i, 64);
+    for (int hb = 0; hb < HB; ++hb) {
+        float l = lsum[hb];
+        l += __shfl_xor(l, 16, 64);
+        l += __shfl_xor(l, 32, 64);
+        const float inv = l > 0.f ? 1.f / l : 0.f;
+        if (lse && grp == 0)
+            lse[(int64_t)g * HQ + head0 + 16 * hb + c16] = l > 0.f ? (m[hb] + log2f(l)) * LN2 : -INFINITY;
+        float iv[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int64_t orow = ((int64_t)g * HQ + head0 + 4 * grp + i) * MLA_DV;
+        for (int i = 0; i < 4; ++i)
+            iv[i] = __shfl(inv, 4 * grp + i, 64);
 #pragma unroll
-        for (int nb = 0; nb < MLA_NB; ++nb) {
-            const float v = o[nb][i] * iv[i];
-            if (out_f32)
-                ((float *)out)[orow + 16 * nb + c16] = v;
-            else
-                ((uint16_t *)out)[orow + 16 * nb + c16] = f32_to_bf16_rne(v);
+        for (int i = 0; i < 4; ++i) {
+            const int64_t orow = ((int64_t)g * HQ + head0 + 16 * hb + 4 * grp + i) * MLA_DV;
+#pragma unroll
+            for (int nb = 0; nb < MLA_NB; ++nb) {
+                const float v = o[hb][nb][i] * iv[i];
+                if (out_f32)
+                    ((float *)out)[orow + 16 * nb + c16] = v;
+                else
+                    ((uint16_t *)out)[orow + 16 * nb + c16] = f32_to_bf16_rne(v);
+            }
         }
     }
 }
@@ -344,13 +374,13 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
                                of32, lse);
         };
         if (Hq == 128)
-            launch(sparse_mla_mfma<8>, 8);
+            launch(sparse_mla_mfma<8, 1>, 8);
         else if (Hq == 64)
-            launch(sparse_mla_mfma<4>, 4);
+            launch(sparse_mla_mfma<4, 1>, 4);
         else if (Hq == 32)
-            launch(sparse_mla_mfma<2>, 2);
+            launch(sparse_mla_mfma<2, 1>, 2);
         else
-            launch(sparse_mla_mfma<1>, 1);
+            launch(sparse_mla_mfma<1, 1>, 1);
         return launch_status();
     }
     if (dqk > VEC_MAX_DQK || dv > 4 * VEC_THREADS)
