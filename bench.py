@@ -145,13 +145,7 @@ def main():
     attn_flop = 2.0 * N * ai.Hq * k * (ai.dqk + ai.dv)
     t_idx = per["index_scores"] * 1e-3
     ach = idx_flop / t_idx
-    traffic = None
-    if os.path.exists(args.traffic):
-        try:
-            tr = json.load(open(args.traffic))
-            traffic = tr.get("bytes_per_launch")
-        except Exception:
-            traffic = None
+    traffic = measured_traffic(args.traffic)
 
     ms_step = wall / args.steps * 1e3
     counts = diff_out[2].cpu().tolist()
@@ -189,6 +183,21 @@ def main():
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows)
     print(json.dumps(rec))
+
+
+def measured_traffic(path):
+    """HBM bytes per launch of the index-scores kernel from the committed
+    FETCH_SIZE / WRITE_SIZE passes, or None when the kernel's sources have
+    changed since those counters were taken."""
+    import hashlib
+    try:
+        tr = json.load(open(path))
+        h = hashlib.sha256()
+        for f in tr["sources"]:
+            h.update(open(os.path.join(ROOT, f), "rb").read())
+        return tr["bytes_per_launch"] if h.hexdigest() == tr["sources_sha256"] else None
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(wl, ai, nrows):
