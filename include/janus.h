@@ -100,9 +100,9 @@ typedef struct {
  *   w       device [total_q, H] fp32, w >= 0
  *   scores  device fp32; row i of session b starts at
  *           scores + score_start[b] + i*(M_b+N_b) and holds M_b+N_b entries.
- * q_dt must equal k_dt.  fp8 and bf16 with d = 128 and H a multiple of 16 run
- * on MFMA; other shapes and fp32 run on a plain vector kernel.
- * Accumulation is fp32.
+ * q_dt must equal k_dt.  fp8 with H = 64 and d = 128 runs on fp8 MFMA (the
+ * head weights are applied in bf16: relative error <= 2^-8 per term); every
+ * other dtype and shape runs on a plain vector kernel.  Accumulation is fp32.
  */
 int janus_index_scores(const janus_batch *b,
                        const void *q, janus_dtype q_dt, const float *q_scale,
@@ -118,7 +118,7 @@ int janus_index_scores(const janus_batch *b,
  *   scores    device, laid out as written by janus_index_scores
  *   topk_idx  device [total_q, k] int32: the selected ids in ascending id
  *             order, then -1 padding.
- * Requires 1 <= k <= 6144 (rows with at most k candidates have no limit).
+ * Requires 1 <= k <= 6144 and max_ctx <= 2^19 (else JANUS_ERR_UNSUPPORTED).
  * No workspace is needed: pass workspace = NULL with *workspace_bytes set to
  * anything, or query it (always 0).
  */
@@ -146,7 +146,8 @@ int janus_topk(const janus_batch *b, const float *scores, int k,
  *   runs       device [2*num_phys_pages] int32: (start, length) pairs,
  *              ascending by start
  *   counts     device [2] int32: {number of pages, number of runs}
- * Requires num_phys_pages <= 2^24 and max_run >= 1.
+ * Requires num_phys_pages <= 2^19 (else JANUS_ERR_UNSUPPORTED) and
+ * max_run >= 1.
  */
 int janus_page_demand(const janus_batch *b, const int32_t *topk_idx, int k,
                       const int32_t *page_table, int pt_ld, int page_size,
@@ -163,7 +164,8 @@ int janus_page_demand(const janus_batch *b, const int32_t *topk_idx, int k,
  *   miss               device [ceil(num_phys_pages/32)] uint32: A & ~P
  *   miss_runs          device [2*num_phys_pages] int32 (start, length) pairs
  *   counts             device [5] int32: {|A|, |P|, |A&P|, |A&~P|, #miss runs}
- * Requires num_phys_pages <= 2^24 and max_run >= 1.
+ * Requires num_phys_pages <= 2^19 (else JANUS_ERR_UNSUPPORTED) and
+ * max_run >= 1.
  */
 int janus_predict_diff(const uint32_t *actual, const uint32_t *predicted,
                        int num_phys_pages, int max_run,
@@ -189,8 +191,10 @@ int janus_predict_diff(const uint32_t *actual, const uint32_t *predicted,
  *   out     device [total_q, Hq, dv], out_dt JANUS_BF16 or JANUS_F32
  *   lse     device [total_q, Hq] fp32, or NULL
  * A row with no valid id gets out = 0 and lse = -inf.  Softmax and
- * accumulation are fp32; products run on bf16 MFMA for Hq a multiple of 32,
- * dqk = 576, dv = 512 and v_pool == k_pool, else on a plain vector kernel.
+ * accumulation are fp32; products run on bf16 MFMA for Hq in {16, 32, 64,
+ * 128}, dqk = 576, dv = 512, v_pool == k_pool, k <= 4096, a row stride that
+ * is a multiple of 8 and 16-byte aligned q and pool; otherwise on a plain
+ * vector kernel (dqk <= 1024, dv <= 1024), else JANUS_ERR_UNSUPPORTED.
  */
 int janus_sparse_attn(const janus_batch *b,
                       const void *q, int Hq, int dqk, int dv,
