@@ -2,56 +2,109 @@
 // causal candidates [0, M+i] of each score row, exact under the strict order
 // (score descending, id ascending).
 //
-// One 512-thread block per row, two blocks per CU.  A row (up to 557 KB at a
-// 128K history) does not fit in LDS, so the block streams it from HBM once,
-// keeping only candidates that beat a running threshold in an LDS buffer of
-// 8192 (key, id) pairs:
-//   1. threshold seed: a strided sample of whole 128-byte lines (1/32 of the
-//      row) is radix-selected for a rank a little above k * (sample share), so
-//      that in expectation ~1.3k elements pass - one extra read of 3% of the
-//      row instead of a second full pass;
-//   2. streaming filter: 16 KB per thread-block step in flight, ballot +
-//      popcount compaction into the LDS buffer;  whenever the buffer could
-//      overflow it is cut to exactly the k best and the threshold is raised to
-//      the k-th best (key, id), so the buffer never loses a member of the
-//      answer;  if the seed was too high (fewer than k passed), the row is
-//      streamed again with no threshold;
+// One 512-thread block per row.  A row (up to 557 KB at a 128K history) does
+// not fit in LDS, so the block streams it from HBM once, keeping only
+// candidates that beat a running threshold in an LDS buffer of CAP (key, id)
+// pairs (CAP = 4096 for k <= 2048, two blocks per CU; else 8192):
+//   1. threshold seed: a strided sample of whole 128-byte lines (1/32 of a
+//      128K row) is radix-selected on its top 16 key bits for a rank a little
+//      above k * (sample share), so that in expectation ~1.3k elements pass;
+//   2. streaming filter: the row moves in 8 KB stages, one float4 per thread,
+//      through a ring of five registers per thread: four stages are in flight
+//      while one is filtered, with one LDS-only barrier per stage.  Each wave
+//      appends its accepted elements with one LDS atomic.  Slots past the
+//      buffer's end are not written; at the next barrier the buffer is cut to
+//      exactly the k best, the threshold rises to the k-th best (key, id), and
+//      the dropped elements - still in their register - are filtered again,
+//      so no member of the answer is ever lost.  If the seed was above the
+//      k-th key (fewer than k passed), the row is streamed again with no
+//      threshold;
 //   3. exact selection: 8-bit-digit radix select on the order-preserving
 //      score key finds the k-th key; ties on it are resolved by a second radix
-//      select on ids (smallest first);
-//   4. ordered output: the winners are set in an LDS bitmap over [0, n) and
-//      written in ascending id order after a block scan of popcounts.
+//      select on ids (smallest first) when they exist;
+//   4. ordered output: the winners are set in an LDS bitmap over [0, n),
+//      turned into ascending ids by a block scan of popcounts and written out
+//      through LDS, coalesced.
 #include "janus_device.hpp"
 #include "janus_host.hpp"
+
+#include <type_traits>
 
 namespace janus {
 
 constexpr int TK_THREADS = 512;
 constexpr int TK_WAVES = TK_THREADS / kWave;
-constexpr int TK_CAP = 8192;                  // LDS candidate buffer entries
-constexpr int TK_STEP = TK_THREADS * 4;       // elements filtered per sub-step
-constexpr int TK_UNROLL = 8;                  // float4 loads in flight per thread
-constexpr int TK_ITER = TK_STEP * TK_UNROLL;  // elements per streaming iteration
-constexpr int TK_MAX_K = TK_CAP - TK_STEP;    // 6144
-constexpr int TK_MAX_N = TK_CAP * 64;         // bitmap of the output step: 2^19 ids
-constexpr int TK_SAMPLE_LINES = 128;          // ~1/32 of a 128K row, in 32-element lines
+constexpr int TK_STAGE4 = TK_THREADS;     // float4 per stage: one per thread
+constexpr int TK_RING = 5;                // register ring depth; TK_RING - 1 stages in flight
+constexpr int TK_MAX_K = 6144;            // with CAP = 8192: >= 2048 free slots after a cut
+constexpr int TK_SMALL_K = 2048;          // with CAP = 4096
+constexpr int TK_SAMPLE_LINES = 128;      // ~1/32 of a 128K row, in 32-element lines
+constexpr int TK_SAMPLE_PT = TK_SAMPLE_LINES * 32 / TK_THREADS;
 
+// Output step: bitmap words per prefix group, and the group prefix plus the
+// staged ids live in `aux` (CAP/4 + max k words).
+constexpr int TK_GROUP = 8;
+constexpr int tk_max_k(int cap) { return cap <= 4096 ? TK_SMALL_K : TK_MAX_K; }
+
+template <int CAP>
 struct TopkShared {
-    uint32_t key[TK_CAP];
-    int32_t id[TK_CAP];
-    uint32_t hist[256];
+    uint32_t key[CAP];
+    int32_t id[CAP];   // directly behind key: the output bitmap spans both
+    int32_t aux[2 * CAP / TK_GROUP + tk_max_k(CAP)];
+    uint32_t hist[2][256];
     int32_t wsum[TK_WAVES];
     int32_t count;
     uint32_t sel_v;
     int32_t sel_rem;
-    uint32_t thr_key;
-    int32_t thr_id;
+    int32_t sel_cnt;
+    uint32_t thr_key;  // accept (key, id) > (thr_key, thr_id) in the strict order:
+    int32_t thr_id;    //   key > thr_key, or key == thr_key and id < thr_id
+    float thr_f;       // thr_key as a score (the same test on floats)
 };
 
 JANUS_DEV uint64_t lanemask_lt() { return (1ull << (threadIdx.x & 63)) - 1ull; }
 
+// Workgroup barrier that orders LDS only.  __syncthreads() also waits for
+// every outstanding global load.
+JANUS_DEV void lds_sync()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Score of an order-preserving key (inverse of score_key).  Keys below that of
+// -inf are not scores; they map to -inf, which only makes a threshold looser.
+JANUS_DEV float key_score(uint32_t key)
+{
+    if (key < 0x007fffffu)
+        return -INFINITY;
+    return __uint_as_float((key & 0x80000000u) ? (key & 0x7fffffffu) : ~key);
+}
+
+// Sets the running threshold (thread 0 only; the caller synchronises).
+template <int CAP>
+JANUS_DEV void set_threshold(TopkShared<CAP> &sm, uint32_t key, int32_t id)
+{
+    sm.thr_key = key;
+    sm.thr_id = key < 0x007fffffu ? 0x7fffffff : id;
+    sm.thr_f = key_score(key);
+}
+
+// Wave-uniform buffer resource over [base, base + bytes): loads past the end
+// return zeros.
+JANUS_DEV __amdgpu_buffer_rsrc_t row_rsrc(const void *base, uint32_t bytes)
+{
+    const uint64_t a = reinterpret_cast<uint64_t>(base);
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)a);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(a >> 32));
+    void *p = reinterpret_cast<void *>(((uint64_t)hi << 32) | lo);
+    return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)__builtin_amdgcn_readfirstlane(bytes), 0x00020000);
+}
+
 // Inclusive prefix sum over the block (TK_THREADS values); also returns the total.
-JANUS_DEV int block_inclusive_scan(TopkShared &sm, int v, int &total)
+template <int CAP>
+JANUS_DEV int block_inclusive_scan(TopkShared<CAP> &sm, int v, int &total)
 {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
@@ -62,7 +115,7 @@ JANUS_DEV int block_inclusive_scan(TopkShared &sm, int v, int &total)
     }
     if (lane == 63)
         sm.wsum[wave] = v;
-    __syncthreads();
+    lds_sync();
     int off = 0, tot = 0;
 #pragma unroll
     for (int w = 0; w < TK_WAVES; ++w) {
@@ -70,7 +123,7 @@ JANUS_DEV int block_inclusive_scan(TopkShared &sm, int v, int &total)
         off += (w < wave) ? s : 0;
         tot += s;
     }
-    __syncthreads();
+    lds_sync();
     total = tot;
     return v + off;
 }
@@ -92,19 +145,29 @@ JANUS_DEV void hist_add(uint32_t *hist, bool on, uint32_t bin)
         atomicAdd(&hist[bin], 1u);
 }
 
-// Radix select over buffer entries [0, cnt) that satisfy pred(e): returns in
-// sm.sel_v the value V (of val(e)) such that fewer than `want` entries have a
-// larger value and at least `want` have a value >= V; sm.sel_rem is how many
-// entries equal to V are needed to make up `want`.
-template <class Val, class Pred>
-JANUS_DEV void radix_select(TopkShared &sm, int cnt, int want, Val val, Pred pred)
+// Radix select over buffer entries [0, cnt) that satisfy pred(e), on the
+// 8-bit digits of val(e) from the top down to the digit at lo_shift: returns
+// in sm.sel_v the prefix V (the value with the lower lo_shift bits cleared)
+// such that fewer than `want` entries have a larger prefix and at least `want`
+// have a prefix >= V; sm.sel_rem is how many entries with prefix V are needed
+// to make up `want`, and sm.sel_cnt how many entries have prefix V.
+// Two barriers per digit: the histograms alternate between two buffers (the
+// idle one is cleared during the other's pass) and one wave ranks the bins.
+template <int CAP, class Val, class Pred>
+JANUS_DEV void radix_select(TopkShared<CAP> &sm, int cnt, int want, Val val, Pred pred, int lo_shift = 0)
 {
+    if (threadIdx.x < 256) {
+        sm.hist[0][threadIdx.x] = 0u;
+        sm.hist[1][threadIdx.x] = 0u;
+    }
+    lds_sync();
     uint32_t prefix = 0, mask = 0;
     int rem = want;
-    for (int shift = 24; shift >= 0; shift -= 8) {
-        for (int t = threadIdx.x; t < 256; t += TK_THREADS)
-            sm.hist[t] = 0;
-        __syncthreads();
+    int buf = 0;
+    for (int shift = 24; shift >= lo_shift; shift -= 8, buf ^= 1) {
+        uint32_t *hist = sm.hist[buf];
+        if (threadIdx.x < 256 && shift < 24)
+            sm.hist[buf ^ 1][threadIdx.x] = 0u;  // read by the previous pass, used by the next
         for (int e0 = 0; e0 < cnt; e0 += TK_THREADS) {
             int e = e0 + threadIdx.x;
             bool on = false;
@@ -113,38 +176,63 @@ JANUS_DEV void radix_select(TopkShared &sm, int cnt, int want, Val val, Pred pre
                 v = val(e);
                 on = (v & mask) == prefix;
             }
-            hist_add(sm.hist, on, (v >> shift) & 255u);
+            hist_add(hist, on, (v >> shift) & 255u);
         }
-        __syncthreads();
-        // suffix sums from bin 255 down, on the first 256 threads
-        int h = threadIdx.x < 256 ? (int)sm.hist[255 - threadIdx.x] : 0;
-        int tot;
-        int incl = block_inclusive_scan(sm, h, tot);
-        if (threadIdx.x < 256 && incl >= rem && incl - h < rem) {
-            sm.sel_v = 255u - threadIdx.x;
-            sm.sel_rem = rem - (incl - h);
+        lds_sync();
+        if (threadIdx.x < 64) {
+            // lane l holds bins 255-4l .. 252-4l; suffix sums from bin 255 down
+            const int l = threadIdx.x;
+            int h[4], sum = 0;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                h[j] = (int)hist[255 - 4 * l - j];
+                sum += h[j];
+            }
+            int incl = sum;
+#pragma unroll
+            for (int o = 1; o < 64; o <<= 1) {
+                const int t = __shfl_up(incl, o, 64);
+                if (l >= o)
+                    incl += t;
+            }
+            int c = incl - sum;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (c < rem && c + h[j] >= rem) {
+                    sm.sel_v = (uint32_t)(255 - 4 * l - j);
+                    sm.sel_rem = rem - c;
+                    sm.sel_cnt = h[j];
+                }
+                c += h[j];
+            }
         }
-        __syncthreads();
+        lds_sync();
         prefix |= sm.sel_v << shift;
         mask |= 255u << shift;
         rem = sm.sel_rem;
-        __syncthreads();
     }
+    lds_sync();  // everyone has read sel_* before thread 0 rewrites them
     if (threadIdx.x == 0) {
         sm.sel_v = prefix;
         sm.sel_rem = rem;
     }
-    __syncthreads();
+    lds_sync();
 }
 
 // Finds the k-th best (key, id) among the cnt buffered candidates:
 // returns T (key) and I (the largest id among the winners with key T).
 // Winners are exactly: key > T, or key == T and id <= I.
-JANUS_DEV void kth_best(TopkShared &sm, int cnt, int k, uint32_t &T, int32_t &I)
+template <int CAP>
+JANUS_DEV void kth_best(TopkShared<CAP> &sm, int cnt, int k, uint32_t &T, int32_t &I)
 {
     radix_select(sm, cnt, k, [&](int e) { return sm.key[e]; }, [&](int) { return true; });
     T = sm.sel_v;
     const int need = sm.sel_rem;  // winners among key == T
+    if (need == sm.sel_cnt) {     // all of them: no tie to break
+        I = 0x7fffffff;
+        lds_sync();
+        return;
+    }
     // Ties on T: the `need` smallest ids win; select the largest of ~id.
     const uint32_t Tl = T;
     radix_select(sm, cnt, need, [&](int e) { return ~(uint32_t)sm.id[e]; },
@@ -152,134 +240,211 @@ JANUS_DEV void kth_best(TopkShared &sm, int cnt, int k, uint32_t &T, int32_t &I)
     I = (int32_t)~sm.sel_v;
 }
 
-// Keep exactly the k winners in the buffer and raise the threshold to them.
-JANUS_DEV void compact(TopkShared &sm, int k)
+// Cuts the buffer to exactly its k best entries, in place and in order, and
+// raises the threshold to the k-th best.
+template <int CAP>
+__device__ __noinline__ void compact(TopkShared<CAP> &sm, int k)
 {
     const int cnt = sm.count;
     uint32_t T;
     int32_t I;
     kth_best(sm, cnt, k, T, I);
-    constexpr int PER = TK_CAP / TK_THREADS;
-    uint32_t kk[PER];
-    int32_t ii[PER];
-    uint32_t keep = 0;
+    int out = 0;
+    // chunks of 4 entries per thread: every chunk is read before any of it is
+    // overwritten, and its destination ends before the next chunk begins
+    for (int c0 = 0; c0 < cnt; c0 += 4 * TK_THREADS) {
+        uint32_t kk[4];
+        int32_t ii[4];
+        uint32_t keep = 0;
 #pragma unroll
-    for (int j = 0; j < PER; ++j) {
-        const int e = threadIdx.x + j * TK_THREADS;
-        kk[j] = 0u;
-        ii[j] = 0;
-        if (e < cnt) {
-            kk[j] = sm.key[e];
-            ii[j] = sm.id[e];
-            if (kk[j] > T || (kk[j] == T && ii[j] <= I))
-                keep |= 1u << j;
+        for (int j = 0; j < 4; ++j) {
+            const int e = c0 + 4 * threadIdx.x + j;
+            kk[j] = 0u;
+            ii[j] = 0;
+            if (e < cnt) {
+                kk[j] = sm.key[e];
+                ii[j] = sm.id[e];
+                if (kk[j] > T || (kk[j] == T && ii[j] <= I))
+                    keep |= 1u << j;
+            }
         }
+        const int nk = __popc(keep);
+        int tot;
+        int pos = out + block_inclusive_scan(sm, nk, tot) - nk;  // its barriers order reads before writes
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (keep & (1u << j)) {
+                sm.key[pos] = kk[j];
+                sm.id[pos] = ii[j];
+                ++pos;
+            }
+        out += tot;
     }
-    const int nk = __popc(keep);
-    int tot;
-    int pos = block_inclusive_scan(sm, nk, tot) - nk;
-#pragma unroll
-    for (int j = 0; j < PER; ++j)
-        if (keep & (1u << j)) {
-            sm.key[pos] = kk[j];
-            sm.id[pos] = ii[j];
-            ++pos;
-        }
     if (threadIdx.x == 0) {
-        sm.count = tot;  // == k
-        sm.thr_key = T;
-        sm.thr_id = I;
+        sm.count = out;  // == k
+        set_threshold(sm, T, I);
     }
-    __syncthreads();
+    lds_sync();
 }
 
-// Appends the accepted (key, id) pairs of this thread's up-to-4 elements.
-JANUS_DEV void append4(TopkShared &sm, const float v[4], int id0, int nvalid, uint32_t tk, int32_t ti)
+// Appends this thread's accepted elements among x[0..3] (ids id0..id0+3, those
+// flagged in pend) and returns the flags of those that found no slot.
+template <int CAP>
+JANUS_DEV uint32_t append4(TopkShared<CAP> &sm, v4f x, uint32_t pend, int id0)
 {
+    const float tf = sm.thr_f;
+    uint32_t acc = 0;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int id = id0 + j;
-        const uint32_t key = score_key(v[j]);
-        const bool acc = j < nvalid && (key > tk || (key == tk && id < ti));
-        const uint64_t m = __ballot(acc);
-        if (m == 0)
-            continue;
-        int base = 0;
-        if ((threadIdx.x & 63) == 0)
-            base = atomicAdd(&sm.count, __popcll(m));
-        base = __shfl(base, 0, 64);
-        if (acc) {
-            const int pos = base + __popcll(m & lanemask_lt());
-            sm.key[pos] = key;
-            sm.id[pos] = id;
+    for (int j = 0; j < 4; ++j)
+        acc |= (x[j] >= tf ? 1u : 0u) << j;
+    acc &= pend;
+    if (__ballot(acc != 0) == 0)
+        return 0u;
+    // an element equal to the threshold passes only with a smaller id
+    const int32_t ti = sm.thr_id;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if (x[j] == tf && id0 + j >= ti)
+            acc &= ~(1u << j);
+    // wave exclusive prefix of the per-lane counts (<= 4), bit-sliced over ballots
+    const int c = __popc(acc);
+    int excl = 0, tot = 0;
+#pragma unroll
+    for (int bit = 0; bit < 3; ++bit) {
+        const uint64_t m = __ballot((c >> bit) & 1);
+        excl += __popcll(m & lanemask_lt()) << bit;
+        tot += __popcll(m) << bit;
+    }
+    int base = 0;
+    if ((threadIdx.x & 63) == 0 && tot > 0)
+        base = atomicAdd(&sm.count, tot);
+    base = __shfl(base, 0, 64);
+    int slot = base + excl;
+    uint32_t dropped = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if (acc & (1u << j)) {
+            if (slot < CAP) {
+                sm.key[slot] = score_key(x[j]);
+                sm.id[slot] = id0 + j;
+            } else {
+                dropped |= 1u << j;
+            }
+            ++slot;
         }
+    return dropped;
+}
+
+// After a barrier: if some elements of the previous stage found no slot, cut
+// the buffer and filter them again (block-uniform loop; rare).
+template <int CAP>
+JANUS_DEV void recover(TopkShared<CAP> &sm, v4f x, uint32_t pend, int id0, int k)
+{
+    while (sm.count > CAP) {
+        lds_sync();
+        if (threadIdx.x == 0)
+            sm.count = CAP;  // every slot below the cap was written
+        lds_sync();
+        compact(sm, k);
+        pend = append4(sm, x, pend, id0);
+        lds_sync();
     }
 }
 
-// One pass over [0, n) of the row, filtering against the running threshold.
-JANUS_DEV void stream_row(TopkShared &sm, const float *__restrict__ row, int n, int k)
+// One pass over [0, n) of the row, filtering against the running threshold;
+// with `seed`, the threshold is first set from a sample of the row.
+template <int CAP>
+JANUS_DEV void stream_row(TopkShared<CAP> &sm, const float *__restrict__ row, int n, int k, bool seed)
 {
-    // scalar head up to 16-byte alignment, then float4 body, then scalar tail
+    static_assert(TK_RING == 5, "the ring is unrolled by hand");
+    // unaligned head (< 4 elements), 16-byte aligned body of float4s, tail (< 4)
     const int head = min(n, (int)(((16 - (reinterpret_cast<uintptr_t>(row) & 15)) & 15) >> 2));
     const int nbody4 = (n - head) >> 2;
     const int tail0 = head + (nbody4 << 2);
-    {
-        if (sm.count + TK_STEP > TK_CAP)
-            compact(sm, k);
-        float v[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
-        int nv = 0, id0 = 0;
+    const __amdgpu_buffer_rsrc_t body = row_rsrc(row + head, 16u * (uint32_t)nbody4);
+    const int nst = (nbody4 + TK_STAGE4 - 1) / TK_STAGE4;
+    // this thread's float4 of stage j (zeros past the body)
+    auto load = [&](int j) {
+        return __builtin_bit_cast(
+            v4f, __builtin_amdgcn_raw_buffer_load_b128(body, 16 * (j * TK_STAGE4 + (int)threadIdx.x), 0, 0));
+    };
+
+    // seed sample and the head/tail elements go to registers first, then the
+    // first stages are put in flight, then the sample is ranked under them
+    const int nlines = n >> 5;
+    const int stride = max(1, nlines / TK_SAMPLE_LINES);
+    const int m = seed ? min(TK_SAMPLE_LINES, nlines) * 32 : 0;
+    float smp[TK_SAMPLE_PT];
+#pragma unroll
+    for (int j = 0; j < TK_SAMPLE_PT; ++j) {
+        const int e = (int)threadIdx.x + j * TK_THREADS;
+        smp[j] = e < m ? row[(((e >> 5) * stride) << 5) + (e & 31)] : 0.f;
+    }
+    // thread 0 takes the head, thread 1 the tail
+    const int ht0 = threadIdx.x == 1 ? tail0 : 0;
+    const int htn = threadIdx.x == 0 ? head : (threadIdx.x == 1 ? n - tail0 : 0);
+    v4f ht;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        ht[j] = j < htn ? row[ht0 + j] : 0.f;
+
+    v4f x0 = load(0), x1 = load(1), x2 = load(2), x3 = load(3), x4;
+
+    if (seed) {
+#pragma unroll
+        for (int j = 0; j < TK_SAMPLE_PT; ++j) {
+            const int e = (int)threadIdx.x + j * TK_THREADS;
+            if (e < m)
+                sm.key[e] = score_key(smp[j]);
+        }
+        lds_sync();
+        // rank ~ 1.3 * k * (m / n) + 8; two digits suffice, since the seed only
+        // has to be at or below the k-th key
+        const int r = min(m, (int)(1.3f * (float)k * (float)m / (float)n) + 8);
+        radix_select(sm, m, r, [&](int e) { return sm.key[e]; }, [&](int) { return true; }, 16);
         if (threadIdx.x == 0) {
-            for (int j = 0; j < head; ++j)
-                v[j] = row[j];
-            nv = head;
-            id0 = 0;
-        } else if (threadIdx.x == 1) {
-            for (int j = 0; j < n - tail0; ++j)
-                v[j] = row[tail0 + j];
-            nv = n - tail0;
-            id0 = tail0;
+            set_threshold(sm, sm.sel_v, 0x7fffffff);  // accept key >= seed
+            sm.count = 0;
         }
-        append4(sm, v, id0, nv, sm.thr_key, sm.thr_id);
-        __syncthreads();
+        lds_sync();
     }
-    const v4f *body = reinterpret_cast<const v4f *>(row + head);
-    const int niter = (nbody4 * 4 + TK_ITER - 1) / TK_ITER;
-    v4f cur[TK_UNROLL];
-#pragma unroll
-    for (int u = 0; u < TK_UNROLL; ++u) {
-        const int v4 = u * TK_THREADS + threadIdx.x;
-        cur[u] = v4 < nbody4 ? body[v4] : v4f{0.f, 0.f, 0.f, 0.f};
+    append4(sm, ht, (1u << htn) - 1u, ht0);  // at most 8 entries: room is certain
+
+    uint32_t drop = 0;  // previous stage's elements that found no slot
+    int drop_id0 = 0;
+    // stage j is filtered from ring register cur; prev held stage j-1 and
+    // receives stage j+4 once j-1's overflow (if any) is settled
+    auto step = [&](v4f &cur, v4f &prev, int j) {
+        lds_sync();
+        if (sm.count > CAP)
+            recover(sm, prev, drop, drop_id0, k);
+        prev = load(j + TK_RING - 1);
+        const int v4 = j * TK_STAGE4 + (int)threadIdx.x;
+        drop_id0 = head + 4 * v4;
+        drop = append4(sm, cur, v4 < nbody4 ? 0xfu : 0u, drop_id0);
+    };
+    // whole turns of the ring (stages past the body are zeros and masked
+    // off), so that the loop has one exit and the ring needs no copies
+    for (int j = 0; j < nst; j += TK_RING) {
+        step(x0, x4, j);
+        step(x1, x0, j + 1);
+        step(x2, x1, j + 2);
+        step(x3, x2, j + 3);
+        step(x4, x3, j + 4);
     }
-    for (int it = 0; it < niter; ++it) {
-        v4f nxt[TK_UNROLL];
-        const int nb = (it + 1) * (TK_ITER / 4);
-#pragma unroll
-        for (int u = 0; u < TK_UNROLL; ++u) {
-            const int v4 = nb + u * TK_THREADS + threadIdx.x;
-            nxt[u] = (it + 1 < niter && v4 < nbody4) ? body[v4] : v4f{0.f, 0.f, 0.f, 0.f};
-        }
-#pragma unroll
-        for (int u = 0; u < TK_UNROLL; ++u) {
-            if (sm.count + TK_STEP > TK_CAP)
-                compact(sm, k);
-            const int v4 = it * (TK_ITER / 4) + u * TK_THREADS + threadIdx.x;
-            const int nv = v4 < nbody4 ? 4 : 0;
-            float v[4] = {cur[u][0], cur[u][1], cur[u][2], cur[u][3]};
-            append4(sm, v, head + 4 * v4, nv, sm.thr_key, sm.thr_id);
-            __syncthreads();
-        }
-#pragma unroll
-        for (int u = 0; u < TK_UNROLL; ++u)
-            cur[u] = nxt[u];
-    }
+    // the last stage's overflow
+    lds_sync();
+    if (sm.count > CAP)
+        recover(sm, x4, drop, drop_id0, k);
 }
 
-__global__ __launch_bounds__(TK_THREADS, 2) void topk_rows(
+template <int CAP>
+__global__ __launch_bounds__(TK_THREADS, CAP <= 4096 ? 4 : 2) void topk_rows(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len,
     const int64_t *__restrict__ score_start, int num_seqs,
     const float *__restrict__ scores, int k, int32_t *__restrict__ topk_idx)
 {
-    __shared__ TopkShared sm;
+    __shared__ TopkShared<CAP> sm;
     const int g = blockIdx.x;
     const int b = session_of_row(q_start, num_seqs, g);
     const int i = g - q_start[b];
@@ -297,50 +462,27 @@ __global__ __launch_bounds__(TK_THREADS, 2) void topk_rows(
     }
     if (threadIdx.x == 0) {
         sm.count = 0;
-        sm.thr_key = 0u;  // accept everything: key > 0, or key == 0 and id < INT_MAX
-        sm.thr_id = 0x7fffffff;
+        set_threshold(sm, 0u, 0x7fffffff);  // accept everything
     }
-    __syncthreads();
+    lds_sync();
 
-    if (n > TK_CAP) {
-        // 1. threshold seed from a sample of whole lines
-        const int nlines = n >> 5;
-        const int stride = max(1, nlines / TK_SAMPLE_LINES);
-        const int nsl = min(TK_SAMPLE_LINES, nlines);
-        const int m = nsl * 32;
-        for (int e = threadIdx.x; e < m; e += TK_THREADS) {
-            const int line = (e >> 5) * stride;
-            sm.key[e] = score_key(row[(line << 5) + (e & 31)]);
-        }
-        __syncthreads();
-        // rank r of the sample ~ 1.3 * k * (m / n) + 8
-        const int r = min(m, (int)(1.3f * (float)k * (float)m / (float)n) + 8);
-        radix_select(sm, m, r, [&](int e) { return sm.key[e]; }, [&](int) { return true; });
-        if (threadIdx.x == 0) {
-            sm.thr_key = sm.sel_v;         // accept key >= seed
-            sm.thr_id = 0x7fffffff;
-            sm.count = 0;
-        }
-        __syncthreads();
-    }
     // 2. one streaming pass (two if the seed was above the k-th key)
-    stream_row(sm, row, n, k);
+    stream_row(sm, row, n, k, n > CAP);
     if (sm.count < k) {
-        __syncthreads();
+        lds_sync();
         if (threadIdx.x == 0) {
             sm.count = 0;
-            sm.thr_key = 0u;
-            sm.thr_id = 0x7fffffff;
+            set_threshold(sm, 0u, 0x7fffffff);
         }
-        __syncthreads();
-        stream_row(sm, row, n, k);
+        lds_sync();
+        stream_row(sm, row, n, k, false);
     }
     // 3. exact k-th best among the buffered candidates
     const int cnt = sm.count;
     uint32_t T;
     int32_t I;
     kth_best(sm, cnt, k, T, I);
-    constexpr int PER = TK_CAP / TK_THREADS;
+    constexpr int PER = CAP / TK_THREADS;
     int32_t win[PER];
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
@@ -353,35 +495,59 @@ __global__ __launch_bounds__(TK_THREADS, 2) void topk_rows(
                 win[j] = id;
         }
     }
-    __syncthreads();
-    // 4. ascending output through an LDS bitmap over [0, n)
-    uint32_t *bm = sm.key;  // reuse: TK_CAP*2 words (the key and id arrays are contiguous)
-    const int nwords = (n + 31) >> 5;
+    lds_sync();
+    // 4. ascending output: the winners are set in an LDS bitmap over [0, n)
+    //    (in the key and id arrays); prefix counts per group of TK_GROUP
+    //    words give each winner its rank, and the ids are staged by rank in
+    //    aux and written out coalesced
+    uint32_t *bm = sm.key;
+    const int nwords = (n + 31) >> 5;  // <= 2 * CAP (checked by the launcher)
     for (int wd = threadIdx.x; wd < nwords; wd += TK_THREADS)
         bm[wd] = 0u;
-    __syncthreads();
+    lds_sync();
 #pragma unroll
     for (int j = 0; j < PER; ++j)
         if (win[j] >= 0)
             atomicOr(&bm[win[j] >> 5], 1u << (win[j] & 31));
-    __syncthreads();
-    const int wpt = (nwords + TK_THREADS - 1) / TK_THREADS;
-    const int w0 = threadIdx.x * wpt;
-    int c = 0;
-    for (int wd = w0; wd < min(nwords, w0 + wpt); ++wd)
-        c += __popc(bm[wd]);
+    lds_sync();
+    constexpr int MAXG = 2 * CAP / TK_GROUP;          // groups of the largest bitmap
+    constexpr int GPT = (MAXG + TK_THREADS - 1) / TK_THREADS;
+    int32_t *grp = sm.aux;                            // exclusive prefix per group
+    int32_t *stage = sm.aux + MAXG;                   // ids by rank
+    const int ngroups = (nwords + TK_GROUP - 1) / TK_GROUP;
+    int gc[GPT], c = 0;
+#pragma unroll
+    for (int u = 0; u < GPT; ++u) {
+        const int g = threadIdx.x * GPT + u;
+        gc[u] = 0;
+        if (g < ngroups)
+#pragma unroll
+            for (int w = 0; w < TK_GROUP; ++w)
+                gc[u] += g * TK_GROUP + w < nwords ? __popc(bm[g * TK_GROUP + w]) : 0;
+        c += gc[u];
+    }
     int tot;
     int pos = block_inclusive_scan(sm, c, tot) - c;
-    for (int wd = w0; wd < min(nwords, w0 + wpt); ++wd) {
-        uint32_t bits = bm[wd];
-        while (bits) {
-            const int bit = __ffs(bits) - 1;
-            bits &= bits - 1;
-            out[pos++] = (wd << 5) + bit;
-        }
+#pragma unroll
+    for (int u = 0; u < GPT; ++u) {
+        const int g = threadIdx.x * GPT + u;
+        if (g < ngroups)
+            grp[g] = pos;
+        pos += gc[u];
     }
-    for (int j = tot + threadIdx.x; j < k; j += TK_THREADS)
-        out[j] = -1;
+    lds_sync();
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+        if (win[j] >= 0) {
+            const int id = win[j], w = id >> 5, g = w / TK_GROUP;
+            int r = grp[g] + __popc(bm[w] & ((1u << (id & 31)) - 1u));
+            for (int w2 = g * TK_GROUP; w2 < w; ++w2)
+                r += __popc(bm[w2]);
+            stage[r] = id;
+        }
+    lds_sync();
+    for (int j = threadIdx.x; j < k; j += TK_THREADS)
+        out[j] = j < tot ? stage[j] : -1;
 }
 
 } // namespace janus
@@ -396,11 +562,16 @@ extern "C" int janus_topk(const janus_batch *bt, const float *scores, int k, int
         *workspace_bytes = 0;
     if (!batch_ok(bt) || !bt->score_start || !scores || !topk_idx || k < 1)
         return JANUS_ERR_INVALID_ARG;
-    if (k > TK_MAX_K || bt->max_ctx > TK_MAX_N)
+    // the output bitmap spans the key and id arrays: max_ctx <= 2 * CAP * 32
+    if (k > TK_MAX_K || bt->max_ctx > 2 * 8192 * 32)
         return JANUS_ERR_UNSUPPORTED;
     if (bt->total_q == 0)
         return JANUS_OK;
-    hipLaunchKernelGGL(topk_rows, dim3(bt->total_q), dim3(TK_THREADS), 0, as_stream(stream), bt->q_start,
-                       bt->hist_len, bt->score_start, bt->num_seqs, scores, k, topk_idx);
+    if (k <= TK_SMALL_K && bt->max_ctx <= 2 * 4096 * 32)
+        hipLaunchKernelGGL(topk_rows<4096>, dim3(bt->total_q), dim3(TK_THREADS), 0, as_stream(stream), bt->q_start,
+                           bt->hist_len, bt->score_start, bt->num_seqs, scores, k, topk_idx);
+    else
+        hipLaunchKernelGGL(topk_rows<8192>, dim3(bt->total_q), dim3(TK_THREADS), 0, as_stream(stream), bt->q_start,
+                           bt->hist_len, bt->score_start, bt->num_seqs, scores, k, topk_idx);
     return launch_status();
 }
