@@ -3,18 +3,28 @@
 // head.  MLA in its absorbed form is the case dqk = 576 (512 latent + 64
 // rope), dv = 512, V = the first 512 elements of each cached row.
 //
-// MFMA kernel (MLA shape): one block per query token, one wave per 16*HB heads.
-// The token's selected rows are gathered through the page table in tiles of
-// 32 into LDS twice: row-major (the A operand of S^T = K Q^T, one 16-byte read
-// per lane) and transposed as key pairs (the B operand of O = P V).  The
-// queries stay in VGPRs for the whole token; S^T is formed so that each lane's
-// outputs are 8 keys of one head, which is exactly an A operand of the P V
-// product, so P never leaves registers.  Softmax is online in fp32 (exp2
-// domain); O accumulates in fp32 MFMA accumulators.
+// MFMA kernel (MLA shape): one block of NW waves per query token.
+//   * The token's selected rows are gathered through the page table, 32 at a
+//     time, straight into LDS (global_load_lds), into a ring of three tile
+//     buffers: while tile t is computed, tiles t+1 and t+2 are in flight.
+//     Waits are counted (vmcnt) and barriers order LDS only, so the gathers
+//     are never drained early.
+//   * Wave w holds the queries of heads 16w..16w+15 in registers and forms
+//     S^T = K Q^T for them from the row-major tile (one 16-byte read per
+//     lane), so that each lane's outputs are 8 keys of one head: exactly an
+//     A operand of the P V product.  Softmax is online in the exp2 domain;
+//     the running max moves only when a logit exceeds it by a slack, and the
+//     cross-lane max reduction runs only then.
+//   * The waves exchange their P fragments (1 KB each) and rescale factors
+//     through LDS, and wave w then computes O for all heads over its own
+//     slice of 512/NW output dims, reading V through the transposing LDS
+//     read (ds_read_b64_tr_b16): each wave reads 1/NW of the tile's V.
+//   * O accumulates in fp32 MFMA accumulators and is normalised at the end.
 #include "janus_device.hpp"
 #include "janus_host.hpp"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace janus {
 
@@ -32,12 +42,26 @@ typedef short v8s16 __attribute__((ext_vector_type(8)));
 constexpr int MLA_CPR = MLA_DQK * 2 / 16;      // 16-byte chunks per cached row (72)
 constexpr int MLA_PCH = MLA_CPR + 2;            // LDS row pitch in chunks: 1184 B reads the K operand conflict-free
 constexpr int MLA_ROWB = MLA_PCH * 16;          // LDS bytes per tile row
-constexpr int MLA_TILE_CH = MLA_KT * MLA_PCH;   // chunks per tile (2336)
+constexpr int MLA_TILE_CH = MLA_KT * MLA_PCH;   // chunks per tile (2368)
 constexpr int MLA_TILE_INS = (MLA_TILE_CH + 63) / 64;  // wave-instructions per tile (37)
 constexpr int MLA_MAX_K = 4096;                 // selected ids per token held in LDS
 constexpr float RESCALE_SLACK = 8.0f;           // log2 headroom before O is rescaled
 
 typedef short v4s16 __attribute__((ext_vector_type(4)));
+
+// s_waitcnt immediate (gfx9 encoding) that waits for vmcnt <= n only.
+constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+
+// Workgroup barrier over LDS that leaves the tile gathers in flight: this
+// wave's LDS operations are complete (lgkmcnt 0), the compiler may move no
+// memory access across it, and no fence drains the outstanding loads.
+JANUS_DEV void lds_barrier()
+{
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+}
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4s16 lds_v4s16;
 
@@ -49,18 +73,35 @@ JANUS_DEV v4s16 lds_read_tr16(const uint8_t *lds_base, int byte_off)
         (lds_v4s16 *)((__attribute__((address_space(3))) uint8_t *)lds_base + byte_off));
 }
 
-template <int NW, int HB>
+// Every wave issues the same number of gather instructions per tile, so a
+// counted wait is exact; instruction slots past the tile's chunks load a
+// dummy chunk into padding.
+template <int NW>
+constexpr int mla_ipw() { return (MLA_TILE_INS + NW - 1) / NW; }
+template <int NW>
+constexpr int mla_buf_bytes() { return NW * mla_ipw<NW>() * 64 * 16; }
+
+template <int NW>
 __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ kv, int64_t row_stride,
     const int32_t *__restrict__ page_table, int pt_ld, int page_shift, const int32_t *__restrict__ topk,
     int k, float scale_log2, void *__restrict__ out, int out_f32, float *__restrict__ lse)
 {
-    constexpr int HW = 16 * HB;  // heads per wave: HB 16-head MFMA blocks
-    constexpr int HQ = HW * NW;
+    constexpr int HQ = 16 * NW;  // one 16-head MFMA block per wave for S and P
     constexpr int NT = 64 * NW;
-    __shared__ __attribute__((aligned(16))) uint8_t sKV[2][MLA_TILE_INS * 64 * 16];
+    constexpr int IPW = mla_ipw<NW>();
+    constexpr int BUF = mla_buf_bytes<NW>();
+    // three tile buffers; tile_step's restrict-qualified pointers let the
+    // compiler see that reading one never waits for the gather into another
+    __shared__ __attribute__((aligned(16))) uint8_t sKV0[BUF];
+    __shared__ __attribute__((aligned(16))) uint8_t sKV1[BUF];
+    __shared__ __attribute__((aligned(16))) uint8_t sKV2[BUF];
     __shared__ int32_t sSlot[MLA_MAX_K];
+    __shared__ v4i sP[NW * 64];      // P fragments: wave w's lane l at 64w + l
+    __shared__ float sAlpha[HQ];     // O rescale factor per head this tile
+    __shared__ int32_t sResc[NW];    // wave w's heads were rescaled this tile
+    __shared__ float sInvL[HQ];      // 1 / softmax denominator per head
 
     const int g = blockIdx.x;
     const int b = session_of_row(q_start, num_seqs, g);
@@ -69,176 +110,241 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int psz_mask = (1 << page_shift) - 1;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int c16 = lane & 15, grp = lane >> 4;
-    const int head0 = HW * wave;
+    const int head0 = 16 * wave;
 
     // physical row of every selected id (-1: padding)
     for (int j = tid; j < k; j += NT) {
         const int s = topk[(int64_t)g * k + j];
         sSlot[j] = (s >= 0 && s <= lim) ? ((pt[s >> page_shift] << page_shift) + (s & psz_mask)) : -1;
     }
-    // queries of head head0 + 16*hb + c16, dims 32*step + 8*grp .. +7
-    v8bf qf[HB][MLA_STEPS];
-#pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + 16 * hb + c16) * MLA_DQK + 8 * grp;
+    // queries of head head0 + c16, dims 32*step + 8*grp .. +7
+    v8bf qf[MLA_STEPS];
+    {
+        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + c16) * MLA_DQK + 8 * grp;
 #pragma unroll
         for (int st = 0; st < MLA_STEPS; ++st)
-            qf[hb][st] = as_v8bf(*(const v4i *)(qr + 32 * st));
+            qf[st] = as_v8bf(*(const v4i *)(qr + 32 * st));
     }
-    v4f o[HB][MLA_NB];
+    // O for all HQ heads (head block hb = rows 16*hb .. 16*hb+15) over this
+    // wave's NBW blocks of 16 output dims, dims 16*(NBW*wave + nl) + c16
+    constexpr int NBW = MLA_NB / NW;
+    v4f o[NW][NBW];
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb)
+    for (int hb = 0; hb < NW; ++hb)
 #pragma unroll
-        for (int nb = 0; nb < MLA_NB; ++nb)
-            o[hb][nb] = v4f{0.f, 0.f, 0.f, 0.f};
-    float m[HB], lsum[HB];  // per head head0 + 16*hb + c16
-#pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        m[hb] = -INFINITY;
-        lsum[hb] = 0.f;
-    }
+        for (int nl = 0; nl < NBW; ++nl)
+            o[hb][nl] = v4f{0.f, 0.f, 0.f, 0.f};
+    float m = -INFINITY, lsum = 0.f;  // head head0 + c16
     __syncthreads();
 
     const int ntiles = (k + MLA_KT - 1) / MLA_KT;
-    // gather of tile t into buffer: wave-instruction j fills LDS chunks 64j .. 64j+63
-    // (chunks 72 and 73 of each row are padding and load a dummy; padding ids load row 0)
-    auto issue = [&](int t, int buf) {
-        for (int j = wave; j < MLA_TILE_INS; j += NW) {
+    // gather of tile t: the wave's instruction i fills LDS chunks 64j .. 64j+63,
+    // j = wave + NW*i (chunks 72 and 73 of each row are padding and load a
+    // dummy; padding ids load row 0; slots past the tile load a dummy too)
+    auto issue = [&](int t, int i0, int i1, uint8_t *__restrict__ dst) {
+#pragma unroll 1
+        for (int i = i0; i < i1; ++i) {
+            const int j = wave + NW * i;
             const int qch = 64 * j + lane;
-            if (qch < MLA_TILE_CH) {
-                const int r = qch / MLA_PCH;
-                int c = qch - r * MLA_PCH;
-                if (c >= MLA_CPR)
-                    c = 0;
-                const int key = MLA_KT * t + r;
-                int slot = key < k ? sSlot[key] : -1;
-                if (slot < 0)
-                    slot = 0;  // padding rows read a real row; their logits are masked
-                const uint16_t *src = kv + (int64_t)slot * row_stride + 8 * c;
-                __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(&sKV[buf][(64 * j) * 16]), 16,
-                                                 0, 0);
+            const int r = qch / MLA_PCH;
+            int c = qch - r * MLA_PCH;
+            if (c >= MLA_CPR)
+                c = 0;
+            const int key = MLA_KT * t + r;
+            int slot = (qch < MLA_TILE_CH && key < k) ? sSlot[key] : -1;
+            if (slot < 0)
+                slot = 0;  // padding rows read a real row; their logits are masked
+            const uint16_t *src = kv + (int64_t)slot * row_stride + 8 * c;
+            __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
+        }
+    };
+
+    // a fixed group of the wave's gather instructions [I0, I1): their slots
+    // are read together, so the group waits for one LDS round trip
+    auto issue_group = [&](auto I0c, auto I1c, int t, uint8_t *__restrict__ dst) {
+        constexpr int I0 = decltype(I0c)::value, I1 = decltype(I1c)::value, NG = I1 - I0;
+        int ln = lane;
+        asm volatile("" : "+v"(ln));  // keep the chunk positions in this loop, not hoisted out of it
+        int slot[NG], cc[NG];
+#pragma unroll
+        for (int u = 0; u < NG; ++u) {
+            const int qch = 64 * (wave + NW * (I0 + u)) + ln;
+            const int r = qch / MLA_PCH;
+            const int c = qch - r * MLA_PCH;
+            const int key = MLA_KT * t + r;
+            slot[u] = (qch < MLA_TILE_CH && key < k) ? sSlot[key] : -1;
+            cc[u] = c >= MLA_CPR ? 0 : c;
+        }
+#pragma unroll
+        for (int u = 0; u < NG; ++u) {
+            const int j = wave + NW * (I0 + u);
+            const int sl = slot[u] < 0 ? 0 : slot[u];  // padding rows read a real row; their logits are masked
+            const uint16_t *src = kv + (int64_t)sl * row_stride + 8 * cc[u];
+            __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
+        }
+    };
+    // the gathers of tile t+2 are spread over the step (with eight waves:
+    // three at its start, two after the P exchange) so that they queue
+    // behind compute instead of stalling the issue of every wave at once
+    constexpr bool SPREAD = IPW == 5;
+    auto issue_part = [&](int t, int part, uint8_t *__restrict__ dst) {
+        if (t + 2 < ntiles) {
+            if constexpr (SPREAD) {
+                if (part == 0)
+                    issue_group(std::integral_constant<int, 0>{}, std::integral_constant<int, 3>{}, t + 2, dst);
+                else
+                    issue_group(std::integral_constant<int, 3>{}, std::integral_constant<int, 5>{}, t + 2, dst);
+            } else if (part == 0) {
+                issue(t + 2, 0, IPW, dst);
             }
         }
     };
-    issue(0, 0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-
-    for (int t = 0; t < ntiles; ++t) {
-        const int buf = t & 1;
-        if (t + 1 < ntiles)
-            issue(t + 1, buf ^ 1);
-        const uint8_t *tile = sKV[buf];
+    auto tile_step = [&](int t, const uint8_t *__restrict__ tile, uint8_t *__restrict__ next) {
+        issue_part(t, 0, next);
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
-        v4f st[2][HB];
+        v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
+        const uint8_t *row0 = tile + c16 * MLA_ROWB + 16 * grp;
+        const uint8_t *row1 = row0 + 16 * MLA_ROWB;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-            for (int hb = 0; hb < HB; ++hb)
-                st[kb][hb] = v4f{0.f, 0.f, 0.f, 0.f};
-            const int r = 16 * kb + c16;
-            const uint8_t *row = tile + r * MLA_ROWB;
-#pragma unroll
-            for (int step = 0; step < MLA_STEPS; ++step) {
-                const v8bf a = as_v8bf(*(const v4i *)(row + 16 * (4 * step + grp)));
-#pragma unroll
-                for (int hb = 0; hb < HB; ++hb)
-                    st[kb][hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, qf[hb][step], st[kb][hb], 0, 0, 0);
-            }
+        for (int step = 0; step < MLA_STEPS; ++step) {
+            const v4i a0 = *(const v4i *)(row0 + 64 * step);
+            const v4i a1 = *(const v4i *)(row1 + 64 * step);
+            st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a0), qf[step], st0, 0, 0, 0);
+            st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a1), qf[step], st1, 0, 0, 0);
         }
-        // online softmax (exp2 domain) with lazy rescaling of O
-        bool okk[2][4];
+        // online softmax (exp2 domain) with lazy rescaling of O.  Valid keys
+        // of the tile come as a 32-bit mask (lanes 32-63 repeat 0-31); this
+        // lane's keys are 16*kb + 4*grp + i
+        const int vkey = MLA_KT * t + (lane & 31);
+        const uint32_t vmask = (uint32_t)__ballot(vkey < k && sSlot[vkey] >= 0) >> (4 * grp);
+        float x[2][4];
+        float mx = -INFINITY;
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const int key = MLA_KT * t + 16 * kb + 4 * grp + i;
-                okk[kb][i] = key < k && sSlot[key] >= 0;
+                const bool ok = (vmask >> (16 * kb + i)) & 1u;
+                x[kb][i] = ok ? (kb ? st1[i] : st0[i]) * scale_log2 : -INFINITY;
+                mx = fmaxf(mx, x[kb][i]);
             }
-        v8bf pa[HB];
-#pragma unroll
-        for (int hb = 0; hb < HB; ++hb) {
-            float x[2][4];
-            float mx = -INFINITY;
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    x[kb][i] = okk[kb][i] ? st[kb][hb][i] * scale_log2 : -INFINITY;
-                    mx = fmaxf(mx, x[kb][i]);
-                }
+        // the running max m is common to a head's four lane groups; it only
+        // moves when some key exceeds it by the slack, which is rare after
+        // the first tiles, so the cross-lane reduction runs only then
+        const bool over = mx > m + RESCALE_SLACK || (m == -INFINITY && mx > -INFINITY);
+        const bool resc = __ballot(over) != 0;
+        if (resc) {
             mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
             mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const bool grow = mx > m[hb] + RESCALE_SLACK || (m[hb] == -INFINITY && mx > -INFINITY);
-            if (__ballot(grow)) {
-                const float mnew = grow ? mx : m[hb];
-                const float alpha = (m[hb] == -INFINITY) ? 0.f : exp2f(m[hb] - mnew);
-                lsum[hb] *= alpha;
-                m[hb] = mnew;
+            const bool grow = mx > m + RESCALE_SLACK || (m == -INFINITY && mx > -INFINITY);
+            const float mnew = grow ? mx : m;
+            const float alpha = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mnew);
+            lsum *= alpha;
+            m = mnew;
+            if (grp == 0)
+                sAlpha[head0 + c16] = alpha;
+        }
+        if (lane == 0)
+            sResc[wave] = resc;
+        float pv[2][4];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                pv[kb][i] = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[kb][i] - m);
+                lsum += pv[kb][i];
+            }
+        const v8bf pa = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
+                             (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
+        sP[64 * wave + lane] = __builtin_bit_cast(v4i, pa);
+        lds_barrier();
+        issue_part(t, 1, next);
+        // O += P V over this wave's output dims for every head.  The P
+        // fragment of head block hb is exactly an A operand (rows: heads
+        // 16*hb + c16; slots: keys 4*grp + i and 16 + 4*grp + i).  V operand:
+        // those keys, lane (r' = c16/4, cc = c16%4) addressing dims
+        // 16*nb + 4*cc .. +3 of its key row
+        const int rr0 = 4 * grp + (c16 >> 2), cc = c16 & 3;
+        const uint8_t *vrow0 = tile + rr0 * MLA_ROWB, *vrow1 = vrow0 + 16 * MLA_ROWB;
+        const int voff = 16 * (cc >> 1) + (cc & 1) * 8;
+        v8bf bv[NBW];
+#pragma unroll
+        for (int nl = 0; nl < NBW; ++nl) {
+            const int nb = NBW * wave + nl;
+            const v4s16 lo = lds_read_tr16(vrow0, voff + 32 * nb);
+            const v4s16 hi = lds_read_tr16(vrow1, voff + 32 * nb);
+            bv[nl] = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+        }
+#pragma unroll
+        for (int hb = 0; hb < NW; ++hb) {
+            if (sResc[hb]) {  // wave-uniform
                 float ai[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    ai[i] = __shfl(alpha, 4 * grp + i, 64);
+                    ai[i] = sAlpha[16 * hb + 4 * grp + i];
 #pragma unroll
-                for (int nb = 0; nb < MLA_NB; ++nb)
+                for (int nl = 0; nl < NBW; ++nl)
 #pragma unroll
                     for (int i = 0; i < 4; ++i)
-                        o[hb][nb][i] *= ai[i];
+                        o[hb][nl][i] *= ai[i];
             }
-            float pv[2][4];
+            const v8bf ph = __builtin_bit_cast(v8bf, sP[64 * hb + lane]);
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    pv[kb][i] = (m[hb] == -INFINITY) ? 0.f : exp2f(x[kb][i] - m[hb]);
-                    lsum[hb] += pv[kb][i];
-                }
-            pa[hb] = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
-                          (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
+            for (int nl = 0; nl < NBW; ++nl)
+                o[hb][nl] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, bv[nl], o[hb][nl], 0, 0, 0);
         }
-        // O += P V; V operand: keys 4*grp + r' (slots 0-3) and 16 + 4*grp + r' (slots 4-7),
-        // lane (r' = c16/4, cc = c16%4) addresses dims 16*nb + 4*cc .. +3 of its key row
-        const int rr0 = 4 * grp + (c16 >> 2), rr1 = 16 + rr0, cc = c16 & 3;
-        const uint8_t *row0 = tile + rr0 * MLA_ROWB, *row1 = tile + rr1 * MLA_ROWB;
-#pragma unroll
-        for (int nb = 0; nb < MLA_NB; ++nb) {
-            const int ch = 2 * nb + (cc >> 1), sub = (cc & 1) * 8;
-            const v4s16 lo = lds_read_tr16(row0, 16 * ch + sub);
-            const v4s16 hi = lds_read_tr16(row1, 16 * ch + sub);
-            const v8bf bv = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
-#pragma unroll
-            for (int hb = 0; hb < HB; ++hb)
-                o[hb][nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa[hb], bv, o[hb][nb], 0, 0, 0);
-        }
-        __builtin_amdgcn_s_waitcnt(0);
-        __syncthreads();
+        // tile t+1 has landed once at most tile t+2's gathers are pending; the
+        // barrier also frees this tile's buffer for the gather of tile t+3
+        if (t + 2 < ntiles)
+            __builtin_amdgcn_s_waitcnt(vmcnt_only(IPW));
+        else
+            __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+        lds_barrier();
+    };
+
+    issue(0, 0, IPW, sKV0);
+    if (ntiles > 1)
+        issue(1, 0, IPW, sKV1);
+    if (ntiles > 1)
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(IPW));
+    else
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+    __syncthreads();
+    for (int t = 0; t < ntiles; ++t) {
+        const int r3 = t % 3;
+        uint8_t *cur = r3 == 0 ? sKV0 : r3 == 1 ? sKV1 : sKV2;
+        uint8_t *nxt = r3 == 0 ? sKV2 : r3 == 1 ? sKV0 : sKV1;
+        tile_step(t, cur, nxt);
     }
-    // normalise and store: O rows are heads head0 + 16*hb + 4*grp + i, column dim 16*nb + c16
-#pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        float l = lsum[hb];
+    // normalise and store: O rows of head block hb are heads 16*hb + 4*grp + i,
+    // column dims 16*(NBW*wave + nl) + c16
+    {
+        float l = lsum;
         l += __shfl_xor(l, 16, 64);
         l += __shfl_xor(l, 32, 64);
-        const float inv = l > 0.f ? 1.f / l : 0.f;
-        if (lse && grp == 0)
-            lse[(int64_t)g * HQ + head0 + 16 * hb + c16] = l > 0.f ? (m[hb] + log2f(l)) * LN2 : -INFINITY;
-        float iv[4];
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            iv[i] = __shfl(inv, 4 * grp + i, 64);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int64_t orow = ((int64_t)g * HQ + head0 + 16 * hb + 4 * grp + i) * MLA_DV;
-#pragma unroll
-            for (int nb = 0; nb < MLA_NB; ++nb) {
-                const float v = o[hb][nb][i] * iv[i];
-                if (out_f32)
-                    ((float *)out)[orow + 16 * nb + c16] = v;
-                else
-                    ((uint16_t *)out)[orow + 16 * nb + c16] = f32_to_bf16_rne(v);
-            }
+        if (grp == 0) {
+            sInvL[head0 + c16] = l > 0.f ? 1.f / l : 0.f;
+            if (lse)
+                lse[(int64_t)g * HQ + head0 + c16] = l > 0.f ? (m + log2f(l)) * LN2 : -INFINITY;
         }
     }
+    __syncthreads();
+#pragma unroll
+    for (int hb = 0; hb < NW; ++hb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int h = 16 * hb + 4 * grp + i;
+            const float inv = sInvL[h];
+            const int64_t orow = ((int64_t)g * HQ + h) * MLA_DV;
+#pragma unroll
+            for (int nl = 0; nl < NBW; ++nl) {
+                const int d = 16 * (NBW * wave + nl) + c16;
+                const float v = o[hb][nl][i] * inv;
+                if (out_f32)
+                    ((float *)out)[orow + d] = v;
+                else
+                    ((uint16_t *)out)[orow + d] = f32_to_bf16_rne(v);
+            }
+        }
 }
 
 // Plain vector kernel for any (Hq, dqk, dv) and separate K/V pools: one
@@ -374,13 +480,13 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
                                of32, lse);
         };
         if (Hq == 128)
-            launch(sparse_mla_mfma<8, 1>, 8);
+            launch(sparse_mla_mfma<8>, 8);
         else if (Hq == 64)
-            launch(sparse_mla_mfma<4, 1>, 4);
+            launch(sparse_mla_mfma<4>, 4);
         else if (Hq == 32)
-            launch(sparse_mla_mfma<2, 1>, 2);
+            launch(sparse_mla_mfma<2>, 2);
         else
-            launch(sparse_mla_mfma<1, 1>, 1);
+            launch(sparse_mla_mfma<1>, 1);
         return launch_status();
     }
     if (dqk > VEC_MAX_DQK || dv > 4 * VEC_THREADS)

@@ -102,7 +102,20 @@ FILLS = {
     "all_zero": lambda rng, b, i, n: np.where(rng.random(n) < 0.5, 0.0, -0.0),
     "few_levels": lambda rng, b, i, n: rng.integers(0, 5, n).astype(np.float64),
     "uniform": lambda rng, b, i, n: rng.random(n),
+    "inf_mix": lambda rng, b, i, n: np.where(rng.random(n) < 0.01, np.inf,
+                                             np.where(rng.random(n) < 0.3, -np.inf, rng.standard_normal(n))),
+    "sample_trap": lambda rng, b, i, n: _sample_trap(rng, n),
 }
+
+
+def _sample_trap(rng, n):
+    """High values exactly where a strided sample of 32-element lines looks
+    (8 per sampled line), too few to fill k: a threshold taken from such a
+    sample sits above the k-th score, which the kernel must detect."""
+    stride = max(1, (n >> 5) // 128)
+    idx = np.arange(n)
+    hot = ((idx >> 5) % stride == 0) & ((idx & 31) < 8)
+    return rng.random(n) + np.where(hot, 10.0, 0.0)
 
 
 @pytest.mark.parametrize("fill", list(FILLS))
