@@ -183,24 +183,29 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
         }
     };
-    // the gathers of tile t+2 are spread over the step (with eight waves:
-    // three at its start, two after the P exchange) so that they queue
-    // behind compute instead of stalling the issue of every wave at once
+    // the gathers of tile t+2 go out one at a time inside the S loop (with
+    // eight waves: at K-steps 0, 4, 8, 12 and 16), so that an issue stalled
+    // behind the gather queue overlaps MFMAs already in flight instead of
+    // holding every wave at the top of the step; other wave counts issue
+    // them all at step 0
     constexpr bool SPREAD = IPW == 5;
     auto issue_part = [&](int t, int part, uint8_t *__restrict__ dst) {
         if (t + 2 < ntiles) {
             if constexpr (SPREAD) {
-                if (part == 0)
-                    issue_group(std::integral_constant<int, 0>{}, std::integral_constant<int, 3>{}, t + 2, dst);
-                else
-                    issue_group(std::integral_constant<int, 3>{}, std::integral_constant<int, 5>{}, t + 2, dst);
+                switch (part) {
+                case 0: issue_group(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{}, t + 2, dst); break;
+                case 1: issue_group(std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, t + 2, dst); break;
+                case 2: issue_group(std::integral_constant<int, 2>{}, std::integral_constant<int, 3>{}, t + 2, dst); break;
+                case 3: issue_group(std::integral_constant<int, 3>{}, std::integral_constant<int, 4>{}, t + 2, dst); break;
+                case 4: issue_group(std::integral_constant<int, 4>{}, std::integral_constant<int, 5>{}, t + 2, dst); break;
+                default: break;
+                }
             } else if (part == 0) {
                 issue(t + 2, 0, IPW, dst);
             }
         }
     };
     auto tile_step = [&](int t, const uint8_t *__restrict__ tile, uint8_t *__restrict__ next) {
-        issue_part(t, 0, next);
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
         v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
         const uint8_t *row0 = tile + c16 * MLA_ROWB + 16 * grp;
@@ -211,6 +216,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             const v4i a1 = *(const v4i *)(row1 + 64 * step);
             st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a0), qf[step], st0, 0, 0, 0);
             st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a1), qf[step], st1, 0, 0, 0);
+            if (step % 4 == 0)
+                issue_part(t, step / 4, next);
         }
         // online softmax (exp2 domain) with lazy rescaling of O.  Valid keys
         // of the tile come as a 32-bit mask (lanes 32-63 repeat 0-31); this
@@ -257,7 +264,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                              (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
         sP[64 * wave + lane] = __builtin_bit_cast(v4i, pa);
         lds_barrier();
-        issue_part(t, 1, next);
+
         // O += P V over this wave's output dims for every head.  The P
         // fragment of head block hb is exactly an A operand (rows: heads
         // 16*hb + c16; slots: keys 4*grp + i and 16 + 4*grp + i).  V operand:
