@@ -49,12 +49,13 @@ def lib():
         L.jo_bf16_value.restype = dbl
         L.jo_index_scores.argtypes = [i32, P, P, P, i32, P, P, i32, P, P, i32, i32, i32, P, P, i64]
         L.jo_topk.argtypes = [i32, P, P, i32, P, P, i64, i32, P]
+        L.jo_topk_sharded.argtypes = [i32, P, P, i32, P, P, i64, i32, i32, i32, P]
         L.jo_page_demand.argtypes = [i32, P, P, P, i32, P, i32, i32, P, i32, P, P, P]
         L.jo_runs.argtypes = [P, i32, i32, P, P]
         L.jo_predict_diff.argtypes = [P, P, i32, i32, P, P, P]
         L.jo_sparse_attn.argtypes = [i32, P, P, i32, P, P, i32, i32, i32, P, P, i64, i64,
                                      P, i32, i32, P, i32, dbl, P, P]
-        for f in ("jo_index_scores", "jo_topk", "jo_page_demand", "jo_runs",
+        for f in ("jo_index_scores", "jo_topk", "jo_topk_sharded", "jo_page_demand", "jo_runs",
                   "jo_predict_diff", "jo_sparse_attn"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -109,6 +110,20 @@ def topk(q_start, hist_len, rows, scores_rows, k):
     rc = lib().jo_topk(len(hist_len), _p(q_start), _p(hist_len), rows.shape[0], _p(rows), _p(sc),
                        sc.shape[1], k, _p(out))
     _check(rc, "topk")
+    return out
+
+
+def topk_sharded(q_start, hist_len, rows, scores_rows, k, shards, align):
+    """Per-shard top-(k/shards) history ids of the given rows (Eq. 3);
+    scores_rows [len(rows), ld] float32.  Returns [len(rows), k]."""
+    q_start = _c(q_start, np.int32)
+    hist_len = _c(hist_len, np.int32)
+    rows = _c(rows, np.int32)
+    sc = _c(scores_rows, np.float32)
+    out = np.empty((rows.shape[0], k), dtype=np.int32)
+    rc = lib().jo_topk_sharded(len(hist_len), _p(q_start), _p(hist_len), rows.shape[0], _p(rows), _p(sc),
+                               sc.shape[1], k, shards, align, _p(out))
+    _check(rc, "topk_sharded")
     return out
 
 

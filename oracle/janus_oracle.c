@@ -21,6 +21,8 @@
  *   - predicted union and corrective reads S \ S_hat: Eq. (2) and the
  *     paragraph after it, Sec. "KV Selection Prediction"; recall and precision
  *     as defined under "Model-aligned prediction distance".
+ *   - synchronization-free parallel prediction over history shards: Eq. (3),
+ *     same section.
  *   - read packing: maximal runs of selected, physically adjacent blocks,
  *     address-ordered, never including unselected blocks: Sec. "Best-effort
  *     read packing".  Runs are additionally split from their low end into
@@ -195,6 +197,58 @@ int jo_topk(int nseq, const int32_t *q_start, const int32_t *hist_len,
         qsort(c, (size_t)n, sizeof(jo_cand), cand_cmp);
         for (int j = 0; j < k; j++)
             out[(int64_t)r * k + j] = (j < n) ? c[j].idx : -1;
+        free(c);
+    }
+    return bad ? -2 : 0;
+}
+
+/*
+ * Synchronization-free sharded prediction (Eq. 3, Sec. "KV Selection
+ * Prediction", parallel prediction): the history [0, M_b) is split into G
+ * contiguous shards C_n of L_b = align * ceil(ceil(M_b / align) / G) tokens
+ * (shard n: [n L_b, min(M_b, (n+1) L_b)); align = page size keeps every page
+ * in one shard), and each shard selects its own top-(k/G) history tokens per
+ * query row, with no exchange between shards.  Only history tokens are
+ * candidates (the equation ranges over the shard's history keys).
+ * out[r * k + n * (k/G) + j]: shard n's selected ids in (score desc, id asc)
+ * order, then -1.  Requires k % G == 0.
+ */
+int jo_topk_sharded(int nseq, const int32_t *q_start, const int32_t *hist_len,
+                    int nrows, const int32_t *rows, const float *scores, int64_t ld,
+                    int k, int G, int align, int32_t *out)
+{
+    if (nseq < 1 || k < 1 || G < 1 || k % G != 0 || align < 1 || nrows < 0)
+        return -1;
+    const int kg = k / G;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int r = 0; r < nrows; r++) {
+        int g = rows[r];
+        if (g < 0 || g >= q_start[nseq]) {
+            bad = 1;
+            continue;
+        }
+        int b = session_of(nseq, q_start, g);
+        int64_t M = hist_len[b];
+        if (M > ld)
+            M = ld;
+        int64_t units = (M + align - 1) / align;
+        int64_t L = (int64_t)align * ((units + G - 1) / G);
+        jo_cand *c = (jo_cand *)malloc(sizeof(jo_cand) * (size_t)(L > 0 ? L : 1));
+        for (int n = 0; n < G; n++) {
+            int64_t lo = (int64_t)n * L, hi = lo + L;
+            if (hi > M)
+                hi = M;
+            int64_t cnt = hi > lo ? hi - lo : 0;
+            for (int64_t s = 0; s < cnt; s++) {
+                double v = (double)scores[(int64_t)r * ld + lo + s];
+                c[s].v = (v == 0.0) ? 0.0 : v; /* -0.0 compares equal to +0.0 */
+                c[s].idx = (int32_t)(lo + s);
+            }
+            qsort(c, (size_t)cnt, sizeof(jo_cand), cand_cmp);
+            for (int j = 0; j < kg; j++)
+                out[(int64_t)r * k + (int64_t)n * kg + j] = (j < cnt) ? c[j].idx : -1;
+        }
         free(c);
     }
     return bad ? -2 : 0;

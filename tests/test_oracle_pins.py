@@ -187,6 +187,69 @@ def test_topk_lexsort_brute_force_with_ties():
         assert sc[i, :n][sel].min() >= sc[i, :n][~sel].max()
 
 
+# ----------------------------------------------------------------------------- sharded prediction (Eq. 3)
+def _shards(M, G, align):
+    L = align * (-(-(-(-M // align)) // G))
+    return [(n * L, min(M, (n + 1) * L)) for n in range(G)]
+
+
+@pytest.mark.parametrize("M,G,align,k", [(1000, 1, 1, 64), (1000, 4, 64, 64), (777, 8, 16, 40), (130, 4, 64, 64),
+                                         (5000, 16, 64, 256)])
+def test_topk_sharded_is_per_shard_lexsort(M, G, align, k):
+    """Each shard's selection is the (score desc, id asc) head of its own
+    history range, by numpy.lexsort; appended tokens are never candidates."""
+    rng = np.random.default_rng(M + G)
+    N = 5
+    sc = rng.integers(0, 9, size=(N, M + N)).astype(np.float32) + rng.standard_normal((N, M + N)).astype(np.float32) * 0.5 * (G % 2)
+    got = oracle.topk_sharded([0, N], [M], np.arange(N), sc, k, G, align)
+    kg = k // G
+    for i in range(N):
+        for n, (lo, hi) in enumerate(_shards(M, G, align)):
+            part = got[i, n * kg:(n + 1) * kg]
+            cnt = max(0, hi - lo)
+            if cnt:
+                order = lo + np.lexsort((np.arange(cnt), -sc[i, lo:hi].astype(np.float64)))
+                exp = order[:kg]
+            else:
+                exp = np.zeros(0, int)
+            assert np.array_equal(part[:len(exp)], exp)
+            assert np.all(part[len(exp):] == -1)
+
+
+def test_topk_sharded_closed_forms():
+    rng = np.random.default_rng(9)
+    M, N, ps = 640, 3, 64
+    sc = rng.standard_normal((N, M + N)).astype(np.float32)
+    # one shard per page and k/G >= page size: every history token is selected
+    got = oracle.topk_sharded([0, N], [M], np.arange(N), sc, 10 * 64, 10, ps)
+    for i in range(N):
+        assert sorted(got[i][got[i] >= 0].tolist()) == list(range(M))
+    # shards are disjoint, page aligned and inside the history
+    got = oracle.topk_sharded([0, N], [M], np.arange(N), sc, 32, 4, ps)
+    for i in range(N):
+        ids = got[i][got[i] >= 0]
+        assert len(set(ids.tolist())) == len(ids) and ids.max() < M
+        for n, (lo, hi) in enumerate(_shards(M, 4, ps)):
+            assert lo % ps == 0
+            part = got[i, n * 8:(n + 1) * 8]
+            assert np.all((part >= lo) & (part < hi))
+    # k not divisible by the shard count is rejected
+    with pytest.raises(ValueError):
+        oracle.topk_sharded([0, N], [M], np.arange(N), sc, 30, 4, ps)
+
+
+def test_topk_sharded_one_shard_is_history_topk():
+    """G = 1 is Eq. 2's selection over the history keys: the top-k of the
+    history part of the row, by torch.topk on distinct values."""
+    rng = np.random.default_rng(10)
+    M, N, k = 500, 6, 50
+    sc = np.stack([rng.permutation(M + N).astype(np.float32) for _ in range(N)])
+    got = oracle.topk_sharded([0, N], [M], np.arange(N), sc, k, 1, 64)
+    for i in range(N):
+        ref = torch.topk(torch.from_numpy(sc[i, :M]), k).indices.numpy()
+        assert np.array_equal(got[i], ref)
+
+
 # ----------------------------------------------------------------------------- page demand, runs, diff
 def test_page_demand_identity_and_permuted_tables():
     wl = make_workload(hist_len=[1000, 700], new_len=[40, 30], H=2, d=8, idx_dtype="f32", k=64, page_size=16, seed=4)
