@@ -127,6 +127,29 @@ int janus_topk(const janus_batch *b, const float *scores, int k,
                void *stream);
 
 /*
+ * Synchronization-free sharded prediction (Eq. 3, Sec. 4.2): the history of
+ * each session is split into num_shards contiguous shards of
+ *   L_b = align * ceil(ceil(M_b / align) / num_shards)
+ * tokens (shard n covers [n L_b, min(M_b, (n+1) L_b)); align = the page size
+ * keeps every page in one shard), and every shard selects its own top
+ * (k / num_shards) history tokens for each appended token, under the same
+ * strict order as janus_topk and with no exchange between shards.  Only
+ * history tokens are candidates.  One shard is Eq. 2's selection over the
+ * history; the union of all shards' selections is what the shards prefetch
+ * together (feed topk_idx to janus_page_demand).
+ *   scores    device, laid out as written by janus_index_scores
+ *   topk_idx  device [total_q, k] int32: slots n*(k/num_shards) ..
+ *             (n+1)*(k/num_shards)-1 hold shard n's ids in ascending order,
+ *             then -1 padding.
+ * Requires num_shards >= 1, k % num_shards == 0 and align >= 1 (else
+ * JANUS_ERR_INVALID_ARG), k / num_shards <= 6144 and max_ctx <= 2^19 (else
+ * JANUS_ERR_UNSUPPORTED).  No workspace, as for janus_topk.
+ */
+int janus_topk_sharded(const janus_batch *b, const float *scores, int k,
+                       int num_shards, int align, int32_t *topk_idx,
+                       void *workspace, size_t *workspace_bytes, void *stream);
+
+/*
  * Page demand (the union of the per-token selections that must be loaded
  * before attention, mapped to pages) and read packing (Sec. 4.3: one read per
  * maximal run of selected, physically adjacent pages; never an unselected

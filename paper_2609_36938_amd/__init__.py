@@ -55,12 +55,13 @@ def lib():
         SZ = ctypes.POINTER(ctypes.c_size_t)
         L.janus_index_scores.argtypes = [BP, P, i32, P, P, i32, P, P, i32, i32, P, P]
         L.janus_topk.argtypes = [BP, P, i32, P, P, SZ, P]
+        L.janus_topk_sharded.argtypes = [BP, P, i32, i32, i32, P, P, SZ, P]
         L.janus_page_demand.argtypes = [BP, P, i32, P, i32, i32, P, i32, i32, P, P, P, P, P, SZ, P]
         L.janus_predict_diff.argtypes = [P, P, i32, i32, P, P, P, P]
         L.janus_sparse_attn.argtypes = [BP, P, i32, i32, i32, P, P, i64, i64, P, i32, i32, P, i32, f32, P, i32,
                                         P, P]
-        for f in ("janus_index_scores", "janus_topk", "janus_page_demand", "janus_predict_diff",
-                  "janus_sparse_attn"):
+        for f in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
+                  "janus_predict_diff", "janus_sparse_attn"):
             getattr(L, f).restype = ctypes.c_int
         L.janus_status_string.argtypes = [ctypes.c_int]
         L.janus_status_string.restype = ctypes.c_char_p
@@ -149,6 +150,18 @@ def topk(batch: Batch, scores, k: int, out=None, stream=None):
     ws = ctypes.c_size_t(0)
     rc = lib().janus_topk(batch.ref, _ptr(scores), int(k), _ptr(out), None, ctypes.byref(ws), _stream(stream))
     _check(rc, "janus_topk")
+    return out
+
+
+def topk_sharded(batch: Batch, scores, k: int, num_shards: int, align: int, out=None, stream=None):
+    """janus_topk_sharded: [total_q, k] int32; slots n*(k/num_shards) .. hold
+    shard n's history ids, ascending, -1 padded."""
+    if out is None:
+        out = torch.empty((batch.total_q, k), dtype=torch.int32, device=scores.device)
+    ws = ctypes.c_size_t(0)
+    rc = lib().janus_topk_sharded(batch.ref, _ptr(scores), int(k), int(num_shards), int(align), _ptr(out), None,
+                                  ctypes.byref(ws), _stream(stream))
+    _check(rc, "janus_topk_sharded")
     return out
 
 

@@ -442,22 +442,33 @@ template <int CAP>
 __global__ __launch_bounds__(TK_THREADS, CAP <= 4096 ? 4 : 2) void topk_rows(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len,
     const int64_t *__restrict__ score_start, int num_seqs,
-    const float *__restrict__ scores, int k, int32_t *__restrict__ topk_idx)
+    const float *__restrict__ scores, int k_row, int32_t *__restrict__ topk_idx, int shards, int align)
 {
     __shared__ TopkShared<CAP> sm;
-    const int g = blockIdx.x;
+    // causal rows (shards == 0): block g selects k_row of [0, M+i];
+    // sharded rows: block g*shards + n selects k_row/shards of history shard n
+    const int g = shards ? blockIdx.x / shards : blockIdx.x;
     const int b = session_of_row(q_start, num_seqs, g);
     const int i = g - q_start[b];
     const int N = q_start[b + 1] - q_start[b];
     const int M = hist_len[b];
     const int ctx = M + N;
-    const int n = M + i + 1;
-    const float *row = scores + score_start[b] + (int64_t)i * ctx;
-    int32_t *out = topk_idx + (int64_t)g * k;
+    int base = 0, n = M + i + 1, k = k_row;
+    int32_t *out = topk_idx + (int64_t)g * k_row;
+    if (shards) {
+        const int sh = blockIdx.x - g * shards;
+        const int units = (M + align - 1) / align;        // pages of the history
+        const int L = align * ((units + shards - 1) / shards);  // tokens per shard
+        base = min(M, sh * L);
+        n = min(M, base + L) - base;
+        k = k_row / shards;
+        out += sh * k;
+    }
+    const float *row = scores + score_start[b] + (int64_t)i * ctx + base;
 
     if (n <= k) {
         for (int j = threadIdx.x; j < k; j += TK_THREADS)
-            out[j] = j < n ? j : -1;
+            out[j] = j < n ? base + j : -1;
         return;
     }
     if (threadIdx.x == 0) {
@@ -547,12 +558,32 @@ __global__ __launch_bounds__(TK_THREADS, CAP <= 4096 ? 4 : 2) void topk_rows(
         }
     lds_sync();
     for (int j = threadIdx.x; j < k; j += TK_THREADS)
-        out[j] = j < tot ? stage[j] : -1;
+        out[j] = j < tot ? base + stage[j] : -1;
 }
 
 } // namespace janus
 
 using namespace janus;
+
+// Launch over total_q rows (shards == 0) or total_q * shards (row, shard) pairs.
+static int launch_topk(const janus_batch *bt, const float *scores, int k, int32_t *topk_idx, int shards,
+                       int align, void *stream)
+{
+    const int kk = shards ? k / shards : k;
+    // the output bitmap spans the key and id arrays: max_ctx <= 2 * CAP * 32
+    if (kk > TK_MAX_K || bt->max_ctx > 2 * 8192 * 32)
+        return JANUS_ERR_UNSUPPORTED;
+    if (bt->total_q == 0)
+        return JANUS_OK;
+    const dim3 grid((unsigned)bt->total_q * (unsigned)(shards ? shards : 1));
+    if (kk <= TK_SMALL_K && bt->max_ctx <= 2 * 4096 * 32)
+        hipLaunchKernelGGL(topk_rows<4096>, grid, dim3(TK_THREADS), 0, as_stream(stream), bt->q_start, bt->hist_len,
+                           bt->score_start, bt->num_seqs, scores, k, topk_idx, shards, align);
+    else
+        hipLaunchKernelGGL(topk_rows<8192>, grid, dim3(TK_THREADS), 0, as_stream(stream), bt->q_start, bt->hist_len,
+                           bt->score_start, bt->num_seqs, scores, k, topk_idx, shards, align);
+    return launch_status();
+}
 
 extern "C" int janus_topk(const janus_batch *bt, const float *scores, int k, int32_t *topk_idx,
                           void *workspace, size_t *workspace_bytes, void *stream)
@@ -562,16 +593,17 @@ extern "C" int janus_topk(const janus_batch *bt, const float *scores, int k, int
         *workspace_bytes = 0;
     if (!batch_ok(bt) || !bt->score_start || !scores || !topk_idx || k < 1)
         return JANUS_ERR_INVALID_ARG;
-    // the output bitmap spans the key and id arrays: max_ctx <= 2 * CAP * 32
-    if (k > TK_MAX_K || bt->max_ctx > 2 * 8192 * 32)
-        return JANUS_ERR_UNSUPPORTED;
-    if (bt->total_q == 0)
-        return JANUS_OK;
-    if (k <= TK_SMALL_K && bt->max_ctx <= 2 * 4096 * 32)
-        hipLaunchKernelGGL(topk_rows<4096>, dim3(bt->total_q), dim3(TK_THREADS), 0, as_stream(stream), bt->q_start,
-                           bt->hist_len, bt->score_start, bt->num_seqs, scores, k, topk_idx);
-    else
-        hipLaunchKernelGGL(topk_rows<8192>, dim3(bt->total_q), dim3(TK_THREADS), 0, as_stream(stream), bt->q_start,
-                           bt->hist_len, bt->score_start, bt->num_seqs, scores, k, topk_idx);
-    return launch_status();
+    return launch_topk(bt, scores, k, topk_idx, 0, 1, stream);
+}
+
+extern "C" int janus_topk_sharded(const janus_batch *bt, const float *scores, int k, int num_shards, int align,
+                                  int32_t *topk_idx, void *workspace, size_t *workspace_bytes, void *stream)
+{
+    (void)workspace;
+    if (workspace_bytes)
+        *workspace_bytes = 0;
+    if (!batch_ok(bt) || !bt->score_start || !scores || !topk_idx || k < 1 || num_shards < 1 ||
+        k % num_shards != 0 || align < 1)
+        return JANUS_ERR_INVALID_ARG;
+    return launch_topk(bt, scores, k, topk_idx, num_shards, align, stream);
 }

@@ -28,8 +28,8 @@ def declared_symbols():
 
 def test_header_declares_the_five_calls():
     syms = declared_symbols()
-    for s in ("janus_index_scores", "janus_topk", "janus_page_demand", "janus_predict_diff",
-              "janus_sparse_attn", "janus_status_string"):
+    for s in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
+              "janus_predict_diff", "janus_sparse_attn", "janus_status_string"):
         assert s in syms
 
 
@@ -78,6 +78,11 @@ def test_invalid_arguments_are_rejected_on_host(L):
     assert ws.value == 0  # top-k needs no workspace
     # k above the supported maximum
     assert L.janus_topk(ctypes.byref(b), FAKE, 7000, FAKE, None, ctypes.byref(ws), None) == 2
+    # sharded top-k: shard count must divide k; align >= 1
+    assert L.janus_topk_sharded(ctypes.byref(b), FAKE, 30, 4, 64, FAKE, None, ctypes.byref(ws), None) == 1
+    assert L.janus_topk_sharded(ctypes.byref(b), FAKE, 32, 0, 64, FAKE, None, ctypes.byref(ws), None) == 1
+    assert L.janus_topk_sharded(ctypes.byref(b), FAKE, 32, 4, 0, FAKE, None, ctypes.byref(ws), None) == 1
+    assert L.janus_topk_sharded(ctypes.byref(b), FAKE, 8 * 7000, 8, 64, FAKE, None, ctypes.byref(ws), None) == 2
     # mismatched indexer dtypes, bad dtype code, bad sizes
     assert L.janus_index_scores(ctypes.byref(b), FAKE, 2, None, FAKE, 1, None, FAKE, 64, 128, FAKE, None) == 2
     assert L.janus_index_scores(ctypes.byref(b), FAKE, 7, None, FAKE, 7, None, FAKE, 64, 128, FAKE, None) == 1
