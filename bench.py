@@ -41,7 +41,7 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=64, help="query rows in the oracle's timed sample")
+    p.add_argument("--cpu-rows", type=int, default=128, help="query rows in the oracle's timed sample")
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "index_scores_traffic.json"))
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (known bytes) for HBM counter calibration")
@@ -149,6 +149,7 @@ def main():
 
     ms_step = wall / args.steps * 1e3
     counts = diff_out[2].cpu().tolist()
+    sharded = sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, pd_out[0], pt, ps, P, mr, k)
     rec = {
         "metric": "new tokens/s per layer (indexer+top-k+sparse attn) at 128K history; % MFMA/HBM peak",
         "value": N * args.steps / wall,
@@ -179,6 +180,7 @@ def main():
             "sparse_attn_frac_bf16_mfma": attn_flop / (per["sparse_attn"] * 1e-3) / PEAK_BF16,
         },
         "demand": {"pages": int(pd_out[3][0]), "runs": int(pd_out[3][1]), "pred_counts": counts},
+        "sharded_prediction": sharded,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows)
@@ -198,6 +200,28 @@ def measured_traffic(path):
         return tr["bytes_per_launch"] if h.hexdigest() == tr["sources_sha256"] else None
     except (OSError, KeyError, ValueError):
         return None
+
+
+def sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, actual_bm, pt, ps, P, mr, k):
+    """Synchronization-free sharded prediction (Eq. 3) of this layer's set from
+    the predicted queries, for several shard counts: the per-shard top-k time
+    (all shards on this GPU; one GPU's share is 1/G of it) and the recall and
+    precision of the predicted page set against the actual one."""
+    janus.index_scores(bt, qp, kI, w, q_scale=sqp, k_scale=sk, scores=scores)
+    res = {}
+    for G in (1, 2, 4, 8):
+        janus.topk_sharded(bt, scores, k, G, ps)  # warm
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        sel = janus.topk_sharded(bt, scores, k, G, ps)
+        e1.record()
+        bm = janus.page_demand(bt, sel, pt, ps, P, mr)[0]
+        c = janus.predict_diff(actual_bm, bm, P, mr)[2].cpu().tolist()
+        torch.cuda.synchronize()
+        a, p, ap = c[0], c[1], c[2]
+        res[str(G)] = {"topk_ms": e0.elapsed_time(e1), "recall": ap / a if a else 1.0,
+                       "precision": ap / p if p else 1.0, "pred_pages": p, "miss_pages": c[3]}
+    return res
 
 
 def cpu_baseline(wl, ai, nrows):
