@@ -45,13 +45,19 @@ def parse():
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "index_scores_traffic.json"))
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (known bytes) for HBM counter calibration")
+    p.add_argument("--record-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                   help="write --traffic from the counter_collection CSVs of a FETCH_SIZE and a WRITE_SIZE "
+                        "rocprofv3 pass over 'bench.py --copy-calibration', then exit (no GPU needed)")
     return p.parse_args()
 
 
 def main():
     args = parse()
+    if args.record_traffic:
+        record_traffic(*args.record_traffic, args.traffic)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path (see DESIGN.md, sharding).",
+        print("bench.py measures one GPU: the library has no multi-GPU path, so --gpus must be 1.",
               file=sys.stderr)
         sys.exit(2)
     import torch
@@ -200,6 +206,49 @@ def measured_traffic(path):
         return tr["bytes_per_launch"] if h.hexdigest() == tr["sources_sha256"] else None
     except (OSError, KeyError, ValueError):
         return None
+
+
+TRAFFIC_SOURCES = ["paper_2609_36938_amd/csrc/index_scores.hip", "paper_2609_36938_amd/csrc/janus_device.hpp"]
+
+
+def record_traffic(fetch_csv, write_csv, out_path):
+    """HBM bytes per launch of the index-scores kernel from one FETCH_SIZE and
+    one WRITE_SIZE pass, each counter scaled by what it reads for the 1 GiB
+    copy (1 GiB read, 1 GiB written) that --copy-calibration adds; stored with
+    the sha256 of the kernel's sources so that a later change voids it."""
+    import csv
+    import hashlib
+
+    def per_kernel(path, counter):
+        acc = {}
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if r["Counter_Name"] == counter:
+                    acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+        return acc
+
+    fetch, write = per_kernel(fetch_csv, "FETCH_SIZE"), per_kernel(write_csv, "WRITE_SIZE")
+    gib_kib = float(1 << 20)
+    copy_f = max(v for k, vs in fetch.items() if "copyBuffer" in k for v in vs)
+    copy_w = max(v for k, vs in write.items() if "copyBuffer" in k for v in vs)
+    fs, ws = round(gib_kib / copy_f, 2), round(gib_kib / copy_w, 2)
+    name = next(k for k in fetch if "index_scores_fp8_mfma" in k)
+    f_kib = float(np.mean(fetch[name]))
+    w_kib = float(np.mean(write[name]))
+    h = hashlib.sha256()
+    for f in TRAFFIC_SOURCES:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    rec = {"kernel": name.split("(")[0].replace("void ", ""),
+           "workload": "history 131072 + 8192 new tokens, 64 heads x 128 fp8",
+           "fetch_kib_raw": f_kib, "write_kib_raw": w_kib, "fetch_scale": fs, "write_scale": ws,
+           "fetch_bytes": f_kib * 1024 * fs, "write_bytes": w_kib * 1024 * ws,
+           "bytes_per_launch": f_kib * 1024 * fs + w_kib * 1024 * ws,
+           "copy_calibration_kib": {"fetch": copy_f, "write": copy_w},
+           "sources": TRAFFIC_SOURCES, "sources_sha256": h.hexdigest()}
+    with open(out_path, "w") as fh:
+        json.dump(rec, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(rec))
 
 
 def sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, actual_bm, pt, ps, P, mr, k):

@@ -13,12 +13,22 @@
 // keys and stores them as one 16-byte write (256 contiguous bytes per token).
 // Key blocks wholly past every token's causal limit skip the MFMAs.
 //
-// Epilogue: the head weights are held as bf16 pairs and each MFMA's four
-// fp32 outputs are rounded to bf16 pairs, clamped at zero with a packed
-// 16-bit integer max (a negative bf16 is a negative int16), and accumulated
-// with v_dot2_f32_bf16 into fp32: 6 VALU ops per 16x16x128 MFMA instead of 8,
-// and half the weight registers.  Every term is non-negative, so the two
-// roundings bound the relative error of a score by 2^-8.
+// Epilogue: the MFMA applies an E8M0 scale of 2^-25 to the query operand, so
+// every product lands in (-1, 1): |q.k| <= 128 * 448 * 448 < 2^25 for any
+// e4m3 inputs.  On that range the clamping form of v_cvt_pk_bf16_f32 (which
+// clamps to [0, 1] after rounding to nearest even) is exactly ReLU followed
+// by the bf16 rounding, so each pair of outputs costs one convert and one
+// v_dot2_f32_bf16 against head weights pre-multiplied by 2^25: 4 VALU ops
+// per 16x16x128 MFMA.  The fp8 MFMA and the VALU do not overlap on this
+// chip, so VALU ops per MFMA bound the kernel.  Every term is non-negative,
+// so the two bf16 roundings bound the relative error of a score by 2^-8.
+//
+// The clamp modifier cannot be requested from the compiler, so the convert
+// is inline assembly; the compiler does not insert the wait states a VALU
+// read of an MFMA result needs ahead of inline assembly, so the four MFMAs
+// of a group are issued from one assembly block that ends with the wait
+// states (12 for an 8-pass fp8 MFMA, what the compiler itself emits) and
+// starts with the one a VALU write of an MFMA source needs.
 #include "janus_device.hpp"
 #include "janus_host.hpp"
 
@@ -46,6 +56,33 @@ JANUS_DEV bool tile_slot(const int32_t *q_start, int num_seqs, int slot, int til
         acc += nt;
     }
     return false;
+}
+
+// E8M0 scales of the query (byte 0: 2^-25) and key (byte 1: 2^0) operands,
+// one register for both (op_sel picks the byte)
+constexpr int IDX_MFMA_SCALES = 0x7f66;
+
+// Four 16x16x128 fp8 MFMAs sharing the key operand, with the query scale
+// 2^-25; the results may be read by any instruction after the block.
+JANUS_DEV void mfma4_fp8_scaled(v4f &c0, v4f &c1, v4f &c2, v4f &c3, const v8i &a0, const v8i &a1,
+                                const v8i &a2, const v8i &a3, const v8i &bk, int scales)
+{
+    asm("s_nop 1\n\t"
+        "v_mfma_scale_f32_16x16x128_f8f6f4 %0, %4, %8, 0, %9, %9 op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
+        "v_mfma_scale_f32_16x16x128_f8f6f4 %1, %5, %8, 0, %9, %9 op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
+        "v_mfma_scale_f32_16x16x128_f8f6f4 %2, %6, %8, 0, %9, %9 op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
+        "v_mfma_scale_f32_16x16x128_f8f6f4 %3, %7, %8, 0, %9, %9 op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
+        "s_nop 11"
+        : "=&v"(c0), "=&v"(c1), "=&v"(c2), "=&v"(c3)
+        : "v"(a0), "v"(a1), "v"(a2), "v"(a3), "v"(bk), "v"(scales));
+}
+
+// (min(max(x,0),1), min(max(y,0),1)) rounded to a bf16 pair.
+JANUS_DEV v2bf clamp01_bf16x2(float x, float y)
+{
+    v2bf r;
+    asm("v_cvt_pk_bf16_f32 %0, %1, %2 clamp" : "=v"(r) : "v"(x), "v"(y));
+    return r;
 }
 
 constexpr int IDX_STAGE = 128;                      // keys per LDS stage (16 KB)
@@ -132,7 +169,8 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     if (key_lo >= ctx)
         return;
     const int key_hi = min(ctx, key_lo + key_chunk);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    // wave index in a scalar register
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int tw0 = tile0 + wave * TPW;
     const bool wave_on = tw0 < N;
     const int r16 = lane & 15, kg = lane >> 4;
@@ -143,11 +181,16 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     const int key_end = min(key_hi, block_lim + 1);
 
     auto issue = [&](int k0, uint8_t *kdst, float *sdst) {
+        // the lane index passes through an empty asm so that its per-lane
+        // address terms are recomputed here each stage instead of being
+        // hoisted out of the key loop and kept live (or spilled) across it
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
         // 16 wave-instructions of 1 KB fill the 16 KB stage; lane L of
         // instruction i fills chunk 64i + L = (row, slot)
 #pragma unroll
         for (int i = wave; i < IDX_STAGE * 8 / 64; i += 4) {
-            const int qch = 64 * i + lane;
+            const int qch = 64 * i + ln;
             const int r = qch >> 3, sl = qch & 7;
             const int c = sl ^ ((r >> 1) & 7);
             int key = k0 + r;
@@ -158,7 +201,7 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
         }
         // the stage's key scales, one dword per lane (two instructions, waves 0 and 1)
         if (k_scale && wave < 2) {
-            const int key = min(k0 + 64 * wave + lane, ctx - 1);
+            const int key = min(k0 + 64 * wave + ln, ctx - 1);
             __builtin_amdgcn_global_load_lds((const void *)(k_scale + kbase + key),
                                              (lds_void_t *)(sdst + 64 * wave), 4, 0, 0);
         }
@@ -184,8 +227,8 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     const int64_t e_row = (int64_t)qrow0 + (e_ok ? e_tok : 0);
     const int hsub = (4 * kg) % RPT;
     // head weights times the token's query scale (a positive factor of every
-    // term), rounded once to bf16 pairs
-    const float sq = q_scale ? q_scale[e_row] : 1.0f;
+    // term) and 2^25 (undoing the MFMA's query scale), rounded once to bf16 pairs
+    const float sq = (q_scale ? q_scale[e_row] : 1.0f) * 0x1p25f;
     v2bf wv[HB][2];
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb) {
@@ -195,7 +238,7 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     }
     const int lim = M + e_tok;  // last causal candidate of this lane's token
     const int wave_lim = M + min(tw0 + TPW - 1, N - 1);
-    const v4f zero = {0.f, 0.f, 0.f, 0.f};
+    int scales = IDX_MFMA_SCALES;
     // this lane's two 16-byte columns (2*kg, 2*kg+1) of LDS row 16*j + r16
     const int g8 = (r16 >> 1) & 7;
     const int off0 = r16 * 128 + 16 * ((2 * kg) ^ g8), off1 = r16 * 128 + 16 * ((2 * kg + 1) ^ g8);
@@ -239,13 +282,11 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
 #pragma unroll
                 for (int h4 = 0; h4 < HB; h4 += 4) {
                     v4f c[4];
-#pragma unroll
-                    for (int u = 0; u < 4; ++u)
-                        c[u] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a[h4 + u], bk, zero, 0, 0, 0, 0, 0, 0);
+                    mfma4_fp8_scaled(c[0], c[1], c[2], c[3], a[h4], a[h4 + 1], a[h4 + 2], a[h4 + 3], bk, scales);
 #pragma unroll
                     for (int u = 0; u < 4; ++u) {
-                        acc0 = __builtin_amdgcn_fdot2_f32_bf16(relu_bf16x2(c[u][0], c[u][1]), wv[h4 + u][0], acc0, false);
-                        acc1 = __builtin_amdgcn_fdot2_f32_bf16(relu_bf16x2(c[u][2], c[u][3]), wv[h4 + u][1], acc1, false);
+                        acc0 = __builtin_amdgcn_fdot2_f32_bf16(clamp01_bf16x2(c[u][0], c[u][1]), wv[h4 + u][0], acc0, false);
+                        acc1 = __builtin_amdgcn_fdot2_f32_bf16(clamp01_bf16x2(c[u][2], c[u][3]), wv[h4 + u][1], acc1, false);
                     }
                 }
                 float r = acc0 + acc1;
