@@ -62,27 +62,65 @@ JANUS_DEV bool tile_slot(const int32_t *q_start, int num_seqs, int slot, int til
 // one register for both (op_sel picks the byte)
 constexpr int IDX_MFMA_SCALES = 0x7f66;
 
-// Four 16x16x128 fp8 MFMAs sharing the key operand, with the query scale
-// 2^-25; the results may be read by any instruction after the block.
-JANUS_DEV void mfma4_fp8_scaled(v4f &c0, v4f &c1, v4f &c2, v4f &c3, const v8i &a0, const v8i &a1,
-                                const v8i &a2, const v8i &a3, const v8i &bk, int scales)
-{
-    asm("s_nop 1\n\t"
-        "v_mfma_scale_f32_16x16x128_f8f6f4 %0, %4, %8, 0, %9, %9 op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
-        "v_mfma_scale_f32_16x16x128_f8f6f4 %1, %5, %8, 0, %9, %9 op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
-        "v_mfma_scale_f32_16x16x128_f8f6f4 %2, %6, %8, 0, %9, %9 op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
-        "v_mfma_scale_f32_16x16x128_f8f6f4 %3, %7, %8, 0, %9, %9 op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
-        "s_nop 11"
-        : "=&v"(c0), "=&v"(c1), "=&v"(c2), "=&v"(c3)
-        : "v"(a0), "v"(a1), "v"(a2), "v"(a3), "v"(bk), "v"(scales));
-}
+// One group of four head tiles against one 16-key block: four 16x16x128
+// fp8 MFMAs sharing the key operand (query scale 2^-25, so every product is
+// below 1 in magnitude), then each pair of outputs clamped to [0, 1] and
+// rounded to bf16 in place - ReLU - and dotted with its bf16 head-weight
+// pair into acc.  The MFMA results live in v[112:127], declared clobbered, so
+// the group is one block whose wait states are written out (the counts the
+// compiler itself emits for these pairs of instructions): two ahead of the
+// MFMAs (a VALU write of one of their sources), twelve after them (an 8-pass
+// MFMA result read by the VALU), at least one between a convert and the dot
+// product that reads its pair (each dot reads a pair converted two
+// instructions earlier; consecutive dots accumulating into one register need
+// none), and three at the end, before any other instruction reads the dot
+// product's result.  FIRST starts the accumulator at zero.
+#define IDX_MFMA(dst, a) \
+    "v_mfma_scale_f32_16x16x128_f8f6f4 " dst ", %[" a "], %[bk], 0, %[sc], %[sc] op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
+#define IDX_HEAD_GROUP(INIT)                                                                         \
+    INIT "s_nop 1\n\t" IDX_MFMA("v[112:115]", "a0") IDX_MFMA("v[116:119]", "a1") IDX_MFMA("v[120:123]", "a2") \
+        IDX_MFMA("v[124:127]", "a3")                                                                  \
+    "s_nop 11\n\t"                                                                                    \
+    "v_cvt_pk_bf16_f32 v112, v112, v113 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v114, v114, v115 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v112, %[w00]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v116, v116, v117 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v114, %[w01]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v118, v118, v119 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v116, %[w10]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v120, v120, v121 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v118, %[w11]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v122, v122, v123 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v120, %[w20]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v124, v124, v125 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v122, %[w21]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v126, v126, v127 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v124, %[w30]\n\t"                                                       \
+    "s_nop 0\n\t"                                                                                     \
+    "v_dot2c_f32_bf16 %[acc], v126, %[w31]\n\t"                                                       \
+    "s_nop 2"
+#define IDX_HEAD_GROUP_INPUTS                                                                          \
+    [a0] "v"(a0), [a1] "v"(a1), [a2] "v"(a2), [a3] "v"(a3), [bk] "v"(bk), [sc] "v"(scales),            \
+        [w00] "v"(w[0][0]), [w01] "v"(w[0][1]), [w10] "v"(w[1][0]), [w11] "v"(w[1][1]), [w20] "v"(w[2][0]), \
+        [w21] "v"(w[2][1]), [w30] "v"(w[3][0]), [w31] "v"(w[3][1])
+#define IDX_HEAD_GROUP_CLOBBERS                                                                       \
+    "v112", "v113", "v114", "v115", "v116", "v117", "v118", "v119", "v120", "v121", "v122", "v123", "v124", \
+        "v125", "v126", "v127"
 
-// (min(max(x,0),1), min(max(y,0),1)) rounded to a bf16 pair.
-JANUS_DEV v2bf clamp01_bf16x2(float x, float y)
+template <bool FIRST>
+JANUS_DEV void head_group(float &acc, const v8i &a0, const v8i &a1, const v8i &a2, const v8i &a3, const v8i &bk,
+                          int scales, const v2bf (*w)[2])
 {
-    v2bf r;
-    asm("v_cvt_pk_bf16_f32 %0, %1, %2 clamp" : "=v"(r) : "v"(x), "v"(y));
-    return r;
+    if (FIRST)
+        asm(IDX_HEAD_GROUP("v_mov_b32 %[acc], 0\n\t")
+            : [acc] "=&v"(acc)
+            : IDX_HEAD_GROUP_INPUTS
+            : IDX_HEAD_GROUP_CLOBBERS);
+    else
+        asm(IDX_HEAD_GROUP("")
+            : [acc] "+v"(acc)
+            : IDX_HEAD_GROUP_INPUTS
+            : IDX_HEAD_GROUP_CLOBBERS);
 }
 
 constexpr int IDX_STAGE = 128;                      // keys per LDS stage (16 KB)
@@ -180,30 +218,27 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     const int block_lim = M + min(tile0 + TOK_TILE - 1, N - 1);
     const int key_end = min(key_hi, block_lim + 1);
 
+    // Key DMA: lane L of wave instruction i (i = wave + 4j, j < 4) fills
+    // 16-byte chunk 64i + L of the stage, i.e. key row 8i + L/8 at slot L%8,
+    // which holds column slot ^ ((row >> 1) & 7) = slot ^ ((4*wave + L/16) & 7).
+    // The lane's byte offset into the stage's keys is therefore fixed, and
+    // the four instructions differ by 4 KB.
+    const uint32_t kvoff = 1024u * wave + 128u * (lane >> 3) + 16u * ((lane & 7) ^ ((4 * wave + (lane >> 4)) & 7));
     auto issue = [&](int k0, uint8_t *kdst, float *sdst) {
-        // the lane index passes through an empty asm so that its per-lane
-        // address terms are recomputed here each stage instead of being
-        // hoisted out of the key loop and kept live (or spilled) across it
-        int ln = lane;
-        asm volatile("" : "+v"(ln));
-        // 16 wave-instructions of 1 KB fill the 16 KB stage; lane L of
-        // instruction i fills chunk 64i + L = (row, slot)
+        // buffer over the keys from k0 on: rows past the context read as
+        // zeros (their scores are never stored)
+        const __amdgpu_buffer_rsrc_t krs =
+            make_buffer_rsrc((void *)(kI + ((kbase + k0) << 7)), (uint32_t)(ctx - k0) << 7);
 #pragma unroll
-        for (int i = wave; i < IDX_STAGE * 8 / 64; i += 4) {
-            const int qch = 64 * i + ln;
-            const int r = qch >> 3, sl = qch & 7;
-            const int c = sl ^ ((r >> 1) & 7);
-            int key = k0 + r;
-            if (key >= ctx)
-                key = ctx - 1;
-            const uint8_t *src = kI + ((kbase + key) << 7) + 16 * c;
-            __builtin_amdgcn_global_load_lds((const void *)src, (lds_void_t *)(kdst + 1024 * i), 16, 0, 0);
-        }
-        // the stage's key scales, one dword per lane (two instructions, waves 0 and 1)
+        for (int j = 0; j < IDX_STAGE * 8 / 64 / IDX_WAVES; ++j)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (lds_void_t *)(kdst + 1024 * (wave + IDX_WAVES * j)), 16,
+                                                     kvoff + 4096u * j, 0, 0, 0);
+        // the stage's key scales, one dword per lane (waves 0 and 1)
         if (k_scale && wave < 2) {
-            const int key = min(k0 + 64 * wave + ln, ctx - 1);
-            __builtin_amdgcn_global_load_lds((const void *)(k_scale + kbase + key),
-                                             (lds_void_t *)(sdst + 64 * wave), 4, 0, 0);
+            const __amdgpu_buffer_rsrc_t srs =
+                make_buffer_rsrc((void *)(k_scale + kbase + k0), (uint32_t)(ctx - k0) << 2);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(srs, (lds_void_t *)(sdst + 64 * wave), 4, 4u * (64 * wave + lane),
+                                                     0, 0, 0);
         }
     };
     if (key_lo < key_end)
@@ -278,18 +313,11 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
                 const uint8_t *rowb = stg + (64 * gsub + 16 * j) * 128;
                 v4i lo = *(const v4i *)(rowb + off0), hi = *(const v4i *)(rowb + off1);
                 const v8i bk = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                float acc0 = 0.f, acc1 = 0.f;
+                float r;
+                head_group<true>(r, a[0], a[1], a[2], a[3], bk, scales, &wv[0]);
 #pragma unroll
-                for (int h4 = 0; h4 < HB; h4 += 4) {
-                    v4f c[4];
-                    mfma4_fp8_scaled(c[0], c[1], c[2], c[3], a[h4], a[h4 + 1], a[h4 + 2], a[h4 + 3], bk, scales);
-#pragma unroll
-                    for (int u = 0; u < 4; ++u) {
-                        acc0 = __builtin_amdgcn_fdot2_f32_bf16(clamp01_bf16x2(c[u][0], c[u][1]), wv[h4 + u][0], acc0, false);
-                        acc1 = __builtin_amdgcn_fdot2_f32_bf16(clamp01_bf16x2(c[u][2], c[u][3]), wv[h4 + u][1], acc1, false);
-                    }
-                }
-                float r = acc0 + acc1;
+                for (int h4 = 4; h4 < HB; h4 += 4)
+                    head_group<false>(r, a[h4], a[h4 + 1], a[h4 + 2], a[h4 + 3], bk, scales, &wv[h4]);
                 if (GPT >= 2)
                     r += xor_lanes16(r);
                 if (GPT >= 4)
@@ -397,7 +425,9 @@ extern "C" int janus_index_scores(const janus_batch *bt, const void *q, janus_dt
         return JANUS_OK;
     hipStream_t st = as_stream(stream);
     const int nseq = bt->num_seqs;
-    if (q_dt == JANUS_FP8_E4M3 && d == 128 && H == 64) {
+    // the MFMA kernel addresses a session's keys and a block's score rows
+    // with 32-bit buffer offsets: contexts up to 2^24 tokens
+    if (q_dt == JANUS_FP8_E4M3 && d == 128 && H == 64 && bt->max_ctx <= (1 << 24)) {
         // key chunks: a multiple of the XCD count, each a whole number of
         // stages and about IDX_KEY_CHUNK keys long
         const int per_xcd_keys = ceil_div(bt->max_ctx, IDX_XCD);
