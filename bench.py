@@ -41,6 +41,7 @@ def parse():
     p.add_argument("--steps", type=int, default=10)
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-decode", action="store_true", help="skip the decode-phase measurement")
     p.add_argument("--cpu-rows", type=int, default=128, help="query rows in the oracle's timed sample")
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "index_scores_traffic.json"))
     p.add_argument("--copy-calibration", action="store_true",
@@ -156,6 +157,7 @@ def main():
     ms_step = wall / args.steps * 1e3
     counts = diff_out[2].cpu().tolist()
     sharded = sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, pd_out[0], pt, ps, P, mr, k)
+    decode = decode_step(janus, torch, max(args.steps, 5)) if not args.no_decode else None
     rec = {
         "metric": "new tokens/s per layer (indexer+top-k+sparse attn) at 128K history; % MFMA/HBM peak",
         "value": N * args.steps / wall,
@@ -187,6 +189,7 @@ def main():
         },
         "demand": {"pages": int(pd_out[3][0]), "runs": int(pd_out[3][1]), "pred_counts": counts},
         "sharded_prediction": sharded,
+        "decode": decode,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows)
@@ -271,6 +274,75 @@ def sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, actual_bm, 
         res[str(G)] = {"topk_ms": e0.elapsed_time(e1), "recall": ap / a if a else 1.0,
                        "precision": ap / p if p else 1.0, "pred_pages": p, "miss_pages": c[3]}
     return res
+
+
+def decode_step(janus, torch, steps):
+    """The decode phase (Sec. 2.2) at one layer: 64 sessions with histories
+    log-uniform in 32K-160K tokens, one new token each.  A step is scores ->
+    top-k -> page demand -> load set (demand minus the resident pages, 90% of
+    the pool) -> attention split over the CUs.  Indexer inputs come from the
+    shared generator; the KV pool (80K pages, 6 GB) and the attention queries
+    are drawn on the GPU from a seeded generator, since nothing here is
+    compared with the oracle."""
+    from workloads import decode_lengths, make_workload, resident_pages
+
+    B, k = 64, 2048
+    M = decode_lengths(B, 32768, 163840, seed=6)
+    wl = make_workload(hist_len=M, new_len=np.ones(B, np.int32), H=64, d=128, idx_dtype="fp8", k=k, seed=6,
+                       w_scale=1.0 / 8, table="permuted", name="decode-64")
+    dev = torch.device("cuda:0")
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    bt = janus.Batch(wl.hist_len, wl.new_len, device=dev)
+    q, kI, w, sq, sk, pt = T(wl.q), T(wl.kI), T(wl.w), T(wl.q_scale), T(wl.k_scale), T(wl.page_table)
+    res = T(resident_pages(wl, p=0.9).view(np.int32))
+    g = torch.Generator(device=dev)
+    g.manual_seed(6)
+    P, ps = wl.num_phys_pages, wl.page_size
+    pool = (torch.randn((P * ps, 576), generator=g, device=dev) / 24.0).to(torch.bfloat16)
+    qa = torch.randn((B, 128, 576), generator=g, device=dev).to(torch.bfloat16)
+    scores = torch.empty(wl.total_scores, dtype=torch.float32, device=dev)
+    sel = torch.empty((B, k), dtype=torch.int32, device=dev)
+    out = torch.empty((B, 128, 512), dtype=torch.bfloat16, device=dev)
+    ws = torch.empty(B * 16 * 128 * 514 * 4, dtype=torch.uint8, device=dev)
+    pd = janus.page_demand(bt, sel, pt, ps, P, wl.max_run)
+    calls = [
+        ("index_scores", lambda: janus.index_scores(bt, q, kI, w, q_scale=sq, k_scale=sk, scores=scores)),
+        ("topk", lambda: janus.topk(bt, scores, k, out=sel)),
+        ("page_demand", lambda: janus.page_demand(bt, sel, pt, ps, P, wl.max_run, out=pd)),
+        ("load_set", lambda: janus.predict_diff(pd[0], res, P, wl.max_run)),
+        ("sparse_attn_split", lambda: janus.sparse_attn_split(bt, qa, pool, pool, pt, ps, sel, 1.0 / 24.0,
+                                                              num_splits=0, dv=512, out=out, workspace=ws)),
+    ]
+    for _, f in calls:  # warm-up
+        f()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        for _, f in calls:
+            f()
+    torch.cuda.synchronize()
+    step_ms = (time.perf_counter() - t0) / steps * 1e3
+    kms = {}
+    for name, f in calls:
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            f()
+        e1.record()
+        torch.cuda.synchronize()
+        kms[name] = e0.elapsed_time(e1) / steps
+    counts = janus.predict_diff(pd[0], res, P, wl.max_run)[2].cpu().tolist()
+    idx_bytes = wl.kI.nbytes + wl.k_scale.nbytes + wl.total_scores * 4
+    gather = B * k * 1152
+    return {
+        "workload": f"{B} decoding sessions, histories log-uniform in 32K-160K (mean {int(M.mean())}), one new "
+                    f"token each, k={k}, 90% of the pool resident",
+        "unit": "decode tokens/s per layer", "value": B / step_ms * 1e3, "ms_per_step": step_ms, "kernels_ms": kms,
+        "index_scores_GBps": idx_bytes / kms["index_scores"] / 1e6,
+        "index_scores_frac_hbm": idx_bytes / kms["index_scores"] / 1e6 / (PEAK_HBM / 1e9),
+        "sparse_attn_gather_GBps_logical": gather / kms["sparse_attn_split"] / 1e6,
+        "demand_pages": counts[0], "load_pages": counts[3],
+    }
 
 
 def cpu_baseline(wl, ai, nrows):

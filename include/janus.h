@@ -6,11 +6,14 @@
  *
  *   janus_index_scores  indexer relevance of every candidate token   (Eq. 1)
  *   janus_topk          the k best candidates per appended token     (Eq. 1)
+ *   janus_topk_sharded  per-shard top-(k/G) over G history shards    (Eq. 3)
  *   janus_page_demand   union of the selections as a page set, plus
  *                       address-ordered runs of adjacent pages       (union after Eq. 1;
  *                                                                     Sec. 4.3 read packing)
  *   janus_predict_diff  corrective-read set: actual minus predicted  (Eq. 2 and after)
  *   janus_sparse_attn   attention over the selected tokens only      (after Eq. 1)
+ *   janus_sparse_attn_split  the same with each row's selection split over
+ *                       several blocks, for few rows (decode, Sec. 2.2)
  *
  * Running index_scores + topk + page_demand on a predicted indexer query
  * (an earlier layer's hidden state through this layer's indexer) gives the
@@ -227,6 +230,35 @@ int janus_sparse_attn(const janus_batch *b,
                       const int32_t *topk_idx, int k, float scale,
                       void *out, janus_dtype out_dt, float *lse,
                       void *stream);
+
+/*
+ * The same attention with each row's selection split into slices that run
+ * as separate blocks, merged afterwards (flash-decoding: every slice keeps
+ * its own max and sum, the merge rescales them to the common max).  Meant
+ * for few rows - the decode phase (Sec. 2.2: an append prefill with one
+ * appended token per session) - where one block per row would leave most of
+ * the GPU idle.  Same arguments and result as janus_sparse_attn, up to the
+ * order of the fp32 sums, plus:
+ *   num_splits       slices per row, 1 .. 16; 0 = one block per compute
+ *                    unit of the current device, ceil(CUs / total_q) (at
+ *                    most one slice per 32 selected ids either way)
+ *   workspace        device scratch of *workspace_bytes bytes, or NULL to
+ *                    query the size (written to *workspace_bytes, nothing
+ *                    launched): total_q * splits * Hq * 514 * 4 bytes, or 0
+ *                    when one slice results.  Too small: JANUS_ERR_WORKSPACE.
+ * Only the MFMA shape of janus_sparse_attn is supported (else
+ * JANUS_ERR_UNSUPPORTED).  Calls on one stream may share a workspace; calls
+ * that overlap in time need their own.
+ */
+int janus_sparse_attn_split(const janus_batch *b,
+                            const void *q, int Hq, int dqk, int dv,
+                            const void *k_pool, const void *v_pool,
+                            int64_t k_row_stride, int64_t v_row_stride,
+                            const int32_t *page_table, int pt_ld, int page_size,
+                            const int32_t *topk_idx, int k, float softmax_scale,
+                            void *out, janus_dtype out_dt, float *lse,
+                            int num_splits, void *workspace, size_t *workspace_bytes,
+                            void *stream);
 
 /* Static description of a status code. */
 const char *janus_status_string(int status);

@@ -60,8 +60,10 @@ def lib():
         L.janus_predict_diff.argtypes = [P, P, i32, i32, P, P, P, P]
         L.janus_sparse_attn.argtypes = [BP, P, i32, i32, i32, P, P, i64, i64, P, i32, i32, P, i32, f32, P, i32,
                                         P, P]
+        L.janus_sparse_attn_split.argtypes = [BP, P, i32, i32, i32, P, P, i64, i64, P, i32, i32, P, i32, f32, P,
+                                              i32, P, i32, P, SZ, P]
         for f in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
-                  "janus_predict_diff", "janus_sparse_attn"):
+                  "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split"):
             getattr(L, f).restype = ctypes.c_int
         L.janus_status_string.argtypes = [ctypes.c_int]
         L.janus_status_string.restype = ctypes.c_char_p
@@ -224,4 +226,34 @@ def sparse_attn(batch: Batch, q, k_pool, v_pool, page_table, page_size: int, top
                                  int(topk_idx.shape[1]), float(scale), _ptr(out), odt[0], _ptr(lse),
                                  _stream(stream))
     _check(rc, "janus_sparse_attn")
+    return out, lse
+
+
+def sparse_attn_split(batch: Batch, q, k_pool, v_pool, page_table, page_size: int, topk_idx, scale: float,
+                      num_splits: int = 0, k_row_stride: Optional[int] = None, v_row_stride: Optional[int] = None,
+                      dv: Optional[int] = None, out_dtype: str = "bf16", want_lse: bool = False, out=None,
+                      lse=None, workspace=None, stream=None):
+    """janus_sparse_attn_split: as sparse_attn, each row's selection split
+    over num_splits blocks (0: the library picks); returns (out, lse or None).
+    workspace: a device uint8 tensor of at least sparse_attn_split_workspace()
+    bytes, or None to allocate one here."""
+    Hq, dqk = int(q.shape[-2]), int(q.shape[-1])
+    krs = int(k_row_stride if k_row_stride is not None else k_pool.shape[-1])
+    vrs = int(v_row_stride if v_row_stride is not None else v_pool.shape[-1])
+    dv = int(dv if dv is not None else (v_pool.shape[-1] if v_pool is not k_pool else dqk))
+    odt = {"bf16": (JANUS_BF16, torch.bfloat16), "f32": (JANUS_F32, torch.float32)}[out_dtype]
+    if out is None:
+        out = torch.empty((batch.total_q, Hq, dv), dtype=odt[1], device=q.device)
+    if want_lse and lse is None:
+        lse = torch.empty((batch.total_q, Hq), dtype=torch.float32, device=q.device)
+    args = (batch.ref, _ptr(q), Hq, dqk, dv, _ptr(k_pool), _ptr(v_pool), krs, vrs, _ptr(page_table),
+            int(page_table.shape[1]), int(page_size), _ptr(topk_idx), int(topk_idx.shape[1]), float(scale), _ptr(out),
+            odt[0], _ptr(lse), int(num_splits))
+    need = ctypes.c_size_t(0)
+    _check(lib().janus_sparse_attn_split(*args, None, ctypes.byref(need), _stream(stream)), "janus_sparse_attn_split")
+    if workspace is None:
+        workspace = torch.empty(max(int(need.value), 1), dtype=torch.uint8, device=q.device)
+    have = ctypes.c_size_t(workspace.numel() * workspace.element_size())
+    rc = lib().janus_sparse_attn_split(*args, _ptr(workspace), ctypes.byref(have), _stream(stream))
+    _check(rc, "janus_sparse_attn_split")
     return out, lse

@@ -408,6 +408,127 @@ __global__ __launch_bounds__(256) void index_scores_vector(
 
 } // namespace janus
 
+namespace janus {
+
+// Decode-shaped batches (every session appends at most DEC_MAXQ tokens, as in
+// the decode phase): the scores are a GEMV over each session's keys, bound
+// by reading the keys once.  Block (key chunk c, session b): the four waves
+// take the chunk's 64-key groups in turn; a wave reads a group's keys (and
+// their scales) straight from global memory one group ahead - each key is
+// used by this block alone, so nothing is staged in LDS - and for every
+// token runs one head group per 16-key block: four 16x16x128 MFMAs (16 heads
+// x 16 keys each) with the clamped-bf16 epilogue of the prefill kernel.  Lane
+// group g then stores 16-key block g of the group: one 256-byte store per
+// token and group.
+constexpr int DEC_MAXQ = 4;
+constexpr int DEC_CHUNK = 4096;   // keys per block
+
+template <int NQ>
+__global__ __launch_bounds__(256, 2) void index_scores_fp8_decode(
+    const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
+    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start,
+    const uint8_t *__restrict__ q, const float *__restrict__ q_scale, const uint8_t *__restrict__ kI,
+    const float *__restrict__ k_scale, const float *__restrict__ w, float *__restrict__ scores)
+{
+    const int b = blockIdx.y;
+    const int qs = q_start[b], N = q_start[b + 1] - qs;
+    const int M = hist_len[b], ctx = M + N;
+    const int c0 = blockIdx.x * DEC_CHUNK;
+    if (N == 0 || c0 >= ctx)
+        return;
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int r16 = lane & 15, kg = lane >> 4;
+    // A operand of token t, head tile hb: row r16 = head 16hb + r16, bytes
+    // 32kg .. 32kg+31; this lane's output rows 4kg .. 4kg+3 are heads
+    // 16hb + 4kg + i, whose weights (times the query scale and 2^25) it holds
+    v8i a[NQ][4];
+    v2bf wv[NQ][4][2];
+#pragma unroll
+    for (int t = 0; t < NQ; ++t) {
+        const bool ok = t < N;
+        const int64_t row = qs + (ok ? t : 0);
+        const float sq = (q_scale ? q_scale[row] : 1.0f) * 0x1p25f;
+#pragma unroll
+        for (int hb = 0; hb < 4; ++hb) {
+            a[t][hb] = ok ? *(const v8i *)(q + ((row * 64 + 16 * hb + r16) << 7) + 32 * kg)
+                          : v8i{0, 0, 0, 0, 0, 0, 0, 0};
+            const v4f tw = *(const v4f *)(w + row * 64 + 16 * hb + 4 * kg);
+            wv[t][hb][0] = __builtin_convertvector((v2f){tw[0] * sq, tw[1] * sq}, v2bf);
+            wv[t][hb][1] = __builtin_convertvector((v2f){tw[2] * sq, tw[3] * sq}, v2bf);
+        }
+    }
+    const int scales = IDX_MFMA_SCALES;
+    // the session's keys (and key scales) from c0 on: rows past the context
+    // read as zeros; its score rows (row t at t * ctx): stores past them drop
+    const int64_t kbase = (int64_t)ctx_start[b] + c0;
+    const __amdgpu_buffer_rsrc_t krs = make_buffer_rsrc((void *)(kI + (kbase << 7)), (uint32_t)(ctx - c0) << 7);
+    const __amdgpu_buffer_rsrc_t ksr =
+        make_buffer_rsrc((void *)(k_scale ? k_scale + kbase : nullptr), k_scale ? (uint32_t)(ctx - c0) << 2 : 0u);
+    const __amdgpu_buffer_rsrc_t srs = make_buffer_rsrc(scores + score_start[b], (uint32_t)(N * ctx) << 2);
+    const int ngroups = (min(DEC_CHUNK, ctx - c0) + 63) / 64;
+
+    struct Group {
+        v4i k[8];   // 16-key block j: key row 16j + r16, bytes 32kg .. +31
+        float ks;   // scale of key 16kg + r16 (the one this lane stores)
+    };
+    auto load = [&](int g, Group &G) {
+        const uint32_t off = (uint32_t)(64 * g + r16) * 128u + 32u * kg;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            G.k[2 * j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(krs, off + 2048u * j, 0, 0));
+            G.k[2 * j + 1] =
+                __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(krs, off + 2048u * j + 16u, 0, 0));
+        }
+        G.ks = k_scale ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                       ksr, (uint32_t)(64 * g + 16 * kg + r16) * 4u, 0, 0))
+                       : 1.0f;
+    };
+    auto compute = [&](int g, const Group &G) {
+        float res[NQ][4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const v8i bk = v8i{G.k[2 * j][0], G.k[2 * j][1], G.k[2 * j][2], G.k[2 * j][3],
+                               G.k[2 * j + 1][0], G.k[2 * j + 1][1], G.k[2 * j + 1][2], G.k[2 * j + 1][3]};
+#pragma unroll
+            for (int t = 0; t < NQ; ++t) {
+                if (t >= N)  // block-uniform
+                    continue;
+                float r;
+                head_group<true>(r, a[t][0], a[t][1], a[t][2], a[t][3], bk, scales, &wv[t][0]);
+                r += xor_lanes16(r);
+                r += __shfl_xor(r, 32, 64);
+                res[t][j] = r;
+            }
+        }
+        const int sl = 64 * g + 16 * kg + r16;  // key (from c0) this lane stores
+        const int s = c0 + sl;
+#pragma unroll
+        for (int t = 0; t < NQ; ++t) {
+            if (t >= N)
+                continue;
+            float v = kg == 0 ? res[t][0] : kg == 1 ? res[t][1] : kg == 2 ? res[t][2] : res[t][3];
+            v = s > M + t ? -INFINITY : v * G.ks;
+            const uint32_t off = s < ctx ? (uint32_t)(t * ctx + s) * 4u : 0x80000000u;
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), srs, off, 0, 0);
+        }
+    };
+    // The prefetch is unconditional (groups past the chunk read zeros through
+    // the descriptor), so the compiler sees the same number of loads after
+    // every group's and can wait for just that group.
+    Group A, B;
+    load(wave, A);
+    for (int g = wave; g < ngroups; g += 8) {
+        load(g + 4, B);
+        compute(g, A);
+        if (g + 4 >= ngroups)
+            break;
+        load(g + 8, A);
+        compute(g + 4, B);
+    }
+}
+
+}  // namespace janus
+
 using namespace janus;
 
 extern "C" int janus_index_scores(const janus_batch *bt, const void *q, janus_dtype q_dt,
@@ -427,6 +548,22 @@ extern "C" int janus_index_scores(const janus_batch *bt, const void *q, janus_dt
     const int nseq = bt->num_seqs;
     // the MFMA kernel addresses a session's keys and a block's score rows
     // with 32-bit buffer offsets: contexts up to 2^24 tokens
+    if (q_dt == JANUS_FP8_E4M3 && d == 128 && H == 64 && bt->max_ctx <= (1 << 24) && bt->max_q <= DEC_MAXQ) {
+        // decode-shaped: one block per (session, 4096-key chunk)
+        const dim3 grid(ceil_div(bt->max_ctx, DEC_CHUNK), nseq);
+        const auto *qq = (const uint8_t *)q;
+        const auto *kk = (const uint8_t *)kI;
+        if (bt->max_q == 1)
+            hipLaunchKernelGGL(index_scores_fp8_decode<1>, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start,
+                               bt->hist_len, bt->score_start, qq, q_scale, kk, k_scale, w, scores);
+        else if (bt->max_q == 2)
+            hipLaunchKernelGGL(index_scores_fp8_decode<2>, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start,
+                               bt->hist_len, bt->score_start, qq, q_scale, kk, k_scale, w, scores);
+        else
+            hipLaunchKernelGGL(index_scores_fp8_decode<4>, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start,
+                               bt->hist_len, bt->score_start, qq, q_scale, kk, k_scale, w, scores);
+        return launch_status();
+    }
     if (q_dt == JANUS_FP8_E4M3 && d == 128 && H == 64 && bt->max_ctx <= (1 << 24)) {
         // key chunks: a multiple of the XCD count, each a whole number of
         // stages and about IDX_KEY_CHUNK keys long

@@ -81,12 +81,13 @@ constexpr int mla_ipw() { return (MLA_TILE_INS + NW - 1) / NW; }
 template <int NW>
 constexpr int mla_buf_bytes() { return NW * mla_ipw<NW>() * 64 * 16; }
 
-template <int NW>
+template <int NW, bool SPLIT>
 __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ kv, int64_t row_stride,
     const int32_t *__restrict__ page_table, int pt_ld, int page_shift, const int32_t *__restrict__ topk,
-    int k, float scale_log2, void *__restrict__ out, int out_f32, float *__restrict__ lse)
+    int k, float scale_log2, void *__restrict__ out, int out_f32, float *__restrict__ lse, int num_splits,
+    float *__restrict__ part)
 {
     constexpr int HQ = 16 * NW;  // one 16-head MFMA block per wave for S and P
     constexpr int NT = 64 * NW;
@@ -103,7 +104,18 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     __shared__ int32_t sResc[NW];    // wave w's heads were rescaled this tile
     __shared__ float sInvL[HQ];      // 1 / softmax denominator per head
 
-    const int g = blockIdx.x;
+    // SPLIT: block (g, sp) is token g, slice sp of its selection (whole
+    // tiles); otherwise block g is token g over its whole selection
+    const int g = SPLIT ? blockIdx.x / num_splits : blockIdx.x;
+    int kl = k;  // ids in this block's slice (may be 0 when split)
+    const int32_t *sel = topk + (int64_t)g * k;
+    if constexpr (SPLIT) {
+        const int sp = blockIdx.x % num_splits;
+        const int tps = ((k + MLA_KT - 1) / MLA_KT + num_splits - 1) / num_splits;
+        const int j0 = min(k, sp * tps * MLA_KT);
+        kl = min(k, j0 + tps * MLA_KT) - j0;
+        sel += j0;
+    }
     const int b = session_of_row(q_start, num_seqs, g);
     const int lim = hist_len[b] + (g - q_start[b]);  // last causal id
     const int32_t *pt = page_table + (int64_t)b * pt_ld;
@@ -113,8 +125,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int head0 = 16 * wave;
 
     // physical row of every selected id (-1: padding)
-    for (int j = tid; j < k; j += NT) {
-        const int s = topk[(int64_t)g * k + j];
+    for (int j = tid; j < kl; j += NT) {
+        const int s = sel[j];
         sSlot[j] = (s >= 0 && s <= lim) ? ((pt[s >> page_shift] << page_shift) + (s & psz_mask)) : -1;
     }
     // queries of head head0 + c16, dims 32*step + 8*grp .. +7
@@ -137,7 +149,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     float m = -INFINITY, lsum = 0.f;  // head head0 + c16
     __syncthreads();
 
-    const int ntiles = (k + MLA_KT - 1) / MLA_KT;
+    const int ntiles = (kl + MLA_KT - 1) / MLA_KT;
     // gather of tile t: the wave's instruction i fills LDS chunks 64j .. 64j+63,
     // j = wave + NW*i (chunks 72 and 73 of each row are padding and load a
     // dummy; padding ids load row 0; slots past the tile load a dummy too)
@@ -151,7 +163,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             if (c >= MLA_CPR)
                 c = 0;
             const int key = MLA_KT * t + r;
-            int slot = (qch < MLA_TILE_CH && key < k) ? sSlot[key] : -1;
+            int slot = (qch < MLA_TILE_CH && key < kl) ? sSlot[key] : -1;
             if (slot < 0)
                 slot = 0;  // padding rows read a real row; their logits are masked
             const uint16_t *src = kv + (int64_t)slot * row_stride + 8 * c;
@@ -172,7 +184,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             const int r = qch / MLA_PCH;
             const int c = qch - r * MLA_PCH;
             const int key = MLA_KT * t + r;
-            slot[u] = (qch < MLA_TILE_CH && key < k) ? sSlot[key] : -1;
+            slot[u] = (qch < MLA_TILE_CH && key < kl) ? sSlot[key] : -1;
             cc[u] = c >= MLA_CPR ? 0 : c;
         }
 #pragma unroll
@@ -223,7 +235,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // of the tile come as a 32-bit mask (lanes 32-63 repeat 0-31); this
         // lane's keys are 16*kb + 4*grp + i
         const int vkey = MLA_KT * t + (lane & 31);
-        const uint32_t vmask = (uint32_t)__ballot(vkey < k && sSlot[vkey] >= 0) >> (4 * grp);
+        const uint32_t vmask = (uint32_t)__ballot(vkey < kl && sSlot[vkey] >= 0) >> (4 * grp);
         float x[2][4];
         float mx = -INFINITY;
 #pragma unroll
@@ -308,7 +320,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         lds_barrier();
     };
 
-    issue(0, 0, IPW, sKV0);
+    if (ntiles > 0)
+        issue(0, 0, IPW, sKV0);
     if (ntiles > 1)
         issue(1, 0, IPW, sKV1);
     if (ntiles > 1)
@@ -321,6 +334,30 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         uint8_t *cur = r3 == 0 ? sKV0 : r3 == 1 ? sKV1 : sKV2;
         uint8_t *nxt = r3 == 0 ? sKV2 : r3 == 1 ? sKV0 : sKV1;
         tile_step(t, cur, nxt);
+    }
+    if constexpr (SPLIT) {
+        // one slice of a split selection: this slice's unnormalised O, and per
+        // head the max it is relative to (exp2 domain) and its sum, for
+        // attn_combine; layout [blocks][HQ][MLA_DV] then [blocks][HQ][2]
+        float l = lsum;
+        l += __shfl_xor(l, 16, 64);
+        l += __shfl_xor(l, 32, 64);
+        if (grp == 0) {
+            float *ml = part + (int64_t)gridDim.x * HQ * MLA_DV + ((int64_t)blockIdx.x * HQ + head0 + c16) * 2;
+            ml[0] = m;
+            ml[1] = l;
+        }
+#pragma unroll
+        for (int hb = 0; hb < NW; ++hb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int h = 16 * hb + 4 * grp + i;
+                float *orow = part + ((int64_t)blockIdx.x * HQ + h) * MLA_DV;
+#pragma unroll
+                for (int nl = 0; nl < NBW; ++nl)
+                    orow[16 * (NBW * wave + nl) + c16] = o[hb][nl][i];
+            }
+        return;
     }
     // normalise and store: O rows of head block hb are heads 16*hb + 4*grp + i,
     // column dims 16*(NBW*wave + nl) + c16
@@ -352,6 +389,51 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                     ((uint16_t *)out)[orow + d] = f32_to_bf16_rne(v);
             }
         }
+}
+
+// Merge of a selection split into S slices (flash-decoding): per (token,
+// head), with slice maxima m_s and sums l_s, M = max m_s, w_s = 2^(m_s - M),
+// O = sum_s w_s O_s / sum_s w_s l_s and lse = (M + log2 sum_s w_s l_s) ln 2.
+// One block per (token, head); thread t handles dims t, t + 256, ...
+constexpr int COMBINE_THREADS = 256;
+constexpr int MAX_SPLITS = 16;
+
+__global__ __launch_bounds__(COMBINE_THREADS) void attn_combine(const float *__restrict__ part, int splits, int Hq,
+                                                                int dv, void *__restrict__ out, int out_f32,
+                                                                float *__restrict__ lse)
+{
+    const int64_t row = blockIdx.x;  // token * Hq + head
+    const int64_t g = row / Hq, h = row % Hq;
+    const int64_t nblk = (int64_t)gridDim.x / Hq * splits;  // slices over all tokens
+    const float *ml = part + nblk * Hq * dv;
+    float ms[MAX_SPLITS], M = -INFINITY;
+#pragma unroll
+    for (int sp = 0; sp < MAX_SPLITS; ++sp) {
+        ms[sp] = sp < splits ? ml[((g * splits + sp) * Hq + h) * 2] : -INFINITY;
+        M = fmaxf(M, ms[sp]);
+    }
+    float L = 0.f;
+#pragma unroll
+    for (int sp = 0; sp < MAX_SPLITS; ++sp) {
+        ms[sp] = (ms[sp] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms[sp] - M);  // the weight w_s
+        if (sp < splits)
+            L += ms[sp] * ml[((g * splits + sp) * Hq + h) * 2 + 1];
+    }
+    const float inv = L > 0.f ? 1.f / L : 0.f;
+    for (int d = threadIdx.x; d < dv; d += COMBINE_THREADS) {
+        float acc = 0.f;
+#pragma unroll
+        for (int sp = 0; sp < MAX_SPLITS; ++sp)
+            if (sp < splits)
+                acc = fmaf(ms[sp], part[((g * splits + sp) * Hq + h) * dv + d], acc);
+        const float v = acc * inv;
+        if (out_f32)
+            ((float *)out)[row * dv + d] = v;
+        else
+            ((uint16_t *)out)[row * dv + d] = f32_to_bf16_rne(v);
+    }
+    if (lse && threadIdx.x == 0)
+        lse[row] = L > 0.f ? (M + log2f(L)) * LN2 : -INFINITY;
 }
 
 // Plain vector kernel for any (Hq, dqk, dv) and separate K/V pools: one
@@ -458,14 +540,70 @@ __global__ __launch_bounds__(VEC_THREADS) void sparse_attn_vector(
 
 using namespace janus;
 
+namespace janus {
+
+// the MLA MFMA kernels cover this shape (V inside the K rows, 16-byte aligned)
+static bool mla_shape(const void *q, int Hq, int dqk, int dv, const void *k_pool, const void *v_pool,
+                      int64_t k_row_stride, int64_t v_row_stride, int k)
+{
+    return dqk == MLA_DQK && dv == MLA_DV && v_pool == k_pool && v_row_stride == k_row_stride &&
+           (k_row_stride % 8) == 0 && (reinterpret_cast<uintptr_t>(k_pool) & 15) == 0 &&
+           (reinterpret_cast<uintptr_t>(q) & 15) == 0 && k <= MLA_MAX_K &&
+           (Hq == 128 || Hq == 64 || Hq == 32 || Hq == 16);
+}
+
+// one launch of the MLA kernel: splits blocks per token, each over one slice
+// of the selection (part = NULL: splits = 1, normalised output)
+static void launch_mla(const janus_batch *bt, const void *q, int Hq, const void *k_pool, int64_t k_row_stride,
+                       const int32_t *page_table, int pt_ld, int shift, const int32_t *topk_idx, int k, float sl2,
+                       void *out, int of32, float *lse, int splits, float *part, hipStream_t st)
+{
+    const auto *qq = (const uint16_t *)q;
+    const auto *kv = (const uint16_t *)k_pool;
+    auto launch = [&](auto kern, int nw) {
+        hipLaunchKernelGGL(kern, dim3(bt->total_q * splits), dim3(64 * nw), 0, st, bt->q_start, bt->hist_len,
+                           bt->num_seqs, qq, kv, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32,
+                           lse, splits, part);
+    };
+    if (part) {
+        if (Hq == 128)
+            launch(sparse_mla_mfma<8, true>, 8);
+        else if (Hq == 64)
+            launch(sparse_mla_mfma<4, true>, 4);
+        else if (Hq == 32)
+            launch(sparse_mla_mfma<2, true>, 2);
+        else
+            launch(sparse_mla_mfma<1, true>, 1);
+    } else {
+        if (Hq == 128)
+            launch(sparse_mla_mfma<8, false>, 8);
+        else if (Hq == 64)
+            launch(sparse_mla_mfma<4, false>, 4);
+        else if (Hq == 32)
+            launch(sparse_mla_mfma<2, false>, 2);
+        else
+            launch(sparse_mla_mfma<1, false>, 1);
+    }
+}
+
+static bool attn_args_ok(const janus_batch *bt, const void *q, int Hq, int dqk, int dv, const void *k_pool,
+                         const void *v_pool, int64_t k_row_stride, int64_t v_row_stride, const int32_t *page_table,
+                         int pt_ld, int page_size, const int32_t *topk_idx, int k, const void *out)
+{
+    return batch_ok(bt) && q && k_pool && v_pool && page_table && topk_idx && out && Hq >= 1 && dqk >= 1 &&
+           dv >= 1 && k >= 1 && pt_ld >= 1 && pow2(page_size) && k_row_stride >= dqk && v_row_stride >= dv;
+}
+
+}  // namespace janus
+
 extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, int dqk, int dv,
                                  const void *k_pool, const void *v_pool, int64_t k_row_stride,
                                  int64_t v_row_stride, const int32_t *page_table, int pt_ld, int page_size,
                                  const int32_t *topk_idx, int k, float scale, void *out, janus_dtype out_dt,
                                  float *lse, void *stream)
 {
-    if (!batch_ok(bt) || !q || !k_pool || !v_pool || !page_table || !topk_idx || !out || Hq < 1 || dqk < 1 ||
-        dv < 1 || k < 1 || pt_ld < 1 || !pow2(page_size) || k_row_stride < dqk || v_row_stride < dv)
+    if (!attn_args_ok(bt, q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, page_table, pt_ld, page_size,
+                      topk_idx, k, out))
         return JANUS_ERR_INVALID_ARG;
     if (out_dt != JANUS_BF16 && out_dt != JANUS_F32)
         return JANUS_ERR_UNSUPPORTED;
@@ -475,25 +613,9 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
     const int shift = __builtin_ctz((unsigned)page_size);
     const float sl2 = scale * LOG2E;
     const int of32 = out_dt == JANUS_F32;
-    const bool mla = dqk == MLA_DQK && dv == MLA_DV && v_pool == k_pool && v_row_stride == k_row_stride &&
-                     (k_row_stride % 8) == 0 && (reinterpret_cast<uintptr_t>(k_pool) & 15) == 0 &&
-                     (reinterpret_cast<uintptr_t>(q) & 15) == 0;
-    if (mla && k <= MLA_MAX_K && (Hq == 128 || Hq == 64 || Hq == 32 || Hq == 16)) {
-        const auto *qq = (const uint16_t *)q;
-        const auto *kv = (const uint16_t *)k_pool;
-        auto launch = [&](auto kern, int nw) {
-            hipLaunchKernelGGL(kern, dim3(bt->total_q), dim3(64 * nw), 0, st, bt->q_start, bt->hist_len,
-                               bt->num_seqs, qq, kv, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out,
-                               of32, lse);
-        };
-        if (Hq == 128)
-            launch(sparse_mla_mfma<8>, 8);
-        else if (Hq == 64)
-            launch(sparse_mla_mfma<4>, 4);
-        else if (Hq == 32)
-            launch(sparse_mla_mfma<2>, 2);
-        else
-            launch(sparse_mla_mfma<1>, 1);
+    if (mla_shape(q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, k)) {
+        launch_mla(bt, q, Hq, k_pool, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32, lse, 1,
+                   nullptr, st);
         return launch_status();
     }
     if (dqk > VEC_MAX_DQK || dv > 4 * VEC_THREADS)
@@ -502,5 +624,62 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
                        bt->hist_len, bt->num_seqs, (const uint16_t *)q, Hq, dqk, dv, (const uint16_t *)k_pool,
                        (const uint16_t *)v_pool, k_row_stride, v_row_stride, page_table, pt_ld, shift, topk_idx, k,
                        sl2, out, of32, lse);
+    return launch_status();
+}
+
+extern "C" int janus_sparse_attn_split(const janus_batch *bt, const void *q, int Hq, int dqk, int dv,
+                                       const void *k_pool, const void *v_pool, int64_t k_row_stride,
+                                       int64_t v_row_stride, const int32_t *page_table, int pt_ld, int page_size,
+                                       const int32_t *topk_idx, int k, float scale, void *out, janus_dtype out_dt,
+                                       float *lse, int num_splits, void *workspace, size_t *workspace_bytes,
+                                       void *stream)
+{
+    if (!attn_args_ok(bt, q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, page_table, pt_ld, page_size,
+                      topk_idx, k, out) ||
+        !workspace_bytes || num_splits < 0 || num_splits > MAX_SPLITS)
+        return JANUS_ERR_INVALID_ARG;
+    if (out_dt != JANUS_BF16 && out_dt != JANUS_F32)
+        return JANUS_ERR_UNSUPPORTED;
+    if (!mla_shape(q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, k))
+        return JANUS_ERR_UNSUPPORTED;
+    // slices: as given, or (0) enough for one block per compute unit (a
+    // block fills a CU's LDS, so more slices only queue a second round), at
+    // most one slice per 32-id tile and MAX_SPLITS
+    int splits = num_splits;
+    if (splits == 0) {
+        int dev = 0, cus = 256;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return JANUS_ERR_DEVICE;
+        const int tq = std::max(bt->total_q, 1);
+        splits = std::min(MAX_SPLITS, std::max(1, (cus + tq - 1) / tq));
+    }
+    splits = std::min(splits, (k + MLA_KT - 1) / MLA_KT);
+    const size_t need =
+        splits > 1 ? (size_t)bt->total_q * splits * Hq * (MLA_DV + 2) * sizeof(float) : (size_t)0;
+    if (!workspace) {
+        *workspace_bytes = need;
+        return JANUS_OK;
+    }
+    if (*workspace_bytes < need)
+        return JANUS_ERR_WORKSPACE;
+    if (bt->total_q == 0)
+        return JANUS_OK;
+    hipStream_t st = as_stream(stream);
+    const int shift = __builtin_ctz((unsigned)page_size);
+    const float sl2 = scale * LOG2E;
+    const int of32 = out_dt == JANUS_F32;
+    if (splits == 1) {
+        launch_mla(bt, q, Hq, k_pool, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32, lse, 1,
+                   nullptr, st);
+        return launch_status();
+    }
+    float *part = static_cast<float *>(workspace);
+    launch_mla(bt, q, Hq, k_pool, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32, lse, splits,
+               part, st);
+    if (hipGetLastError() != hipSuccess)
+        return JANUS_ERR_DEVICE;
+    hipLaunchKernelGGL(attn_combine, dim3((int64_t)bt->total_q * Hq), dim3(COMBINE_THREADS), 0, st, part, splits, Hq,
+                       MLA_DV, out, of32, lse);
     return launch_status();
 }

@@ -29,7 +29,7 @@ def declared_symbols():
 def test_header_declares_the_five_calls():
     syms = declared_symbols()
     for s in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
-              "janus_predict_diff", "janus_sparse_attn", "janus_status_string"):
+              "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split", "janus_status_string"):
         assert s in syms
 
 
@@ -102,6 +102,32 @@ def test_invalid_arguments_are_rejected_on_host(L):
                                8, ctypes.c_float(0.1), FAKE, 2, None, None) == 2
     assert L.janus_sparse_attn(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 500, 576, FAKE, 4, 64, FAKE,
                                8, ctypes.c_float(0.1), FAKE, 1, None, None) == 1
+
+
+def test_split_attention_workspace_and_rejections(L):
+    """janus_sparse_attn_split: the workspace query (nothing launched with an
+    explicit slice count), a short workspace, and argument errors."""
+    b = _batch()  # total_q rows of the host-only batch
+    f = ctypes.c_float(0.1)
+
+    def call(nsplit, ws, ws_bytes, Hq=128, dqk=576, dv=512, k=2048, v=FAKE, odt=1):
+        return L.janus_sparse_attn_split(ctypes.byref(b), FAKE, Hq, dqk, dv, FAKE, v, 576, 576, FAKE, 4, 64, FAKE, k,
+                                         f, FAKE, odt, None, nsplit, ws, ctypes.byref(ws_bytes), None)
+
+    need = ctypes.c_size_t(0)
+    assert call(4, None, need) == 0
+    assert need.value == b.total_q * 4 * 128 * 514 * 4
+    assert call(1, None, need) == 0 and need.value == 0          # one slice: no workspace
+    assert call(16, None, need, k=64) == 0                        # at most one slice per 32 ids
+    assert need.value == b.total_q * 2 * 128 * 514 * 4
+    short = ctypes.c_size_t(b.total_q * 4 * 128 * 514 * 4 - 1)
+    assert call(4, FAKE, short) == 3                              # JANUS_ERR_WORKSPACE
+    assert call(17, None, need) == 1 and call(-1, None, need) == 1
+    assert L.janus_sparse_attn_split(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 576, 576, FAKE, 4, 64, FAKE,
+                                     8, f, FAKE, 1, None, 2, None, None, None) == 1  # no size pointer
+    assert call(2, None, need, dqk=128, dv=128) == 2              # only the MFMA shape splits
+    assert call(2, None, need, v=ctypes.c_void_p(0x2000)) == 2    # separate V pool
+    assert call(2, None, need, odt=2) == 2                        # fp8 output
 
 
 def test_product_path_does_not_touch_the_oracle():

@@ -425,3 +425,33 @@ def test_attention_closed_forms():
     c_, _ = oracle.sparse_attn(wl.q_start, wl.hist_len, rows, ai.q, ai.k_pool, ai.v_pool, ai.k_row_stride,
                                ai.v_row_stride, wl.page_table, wl.page_size, sel2[:, :9], ai.scale, ai.dv)
     assert np.allclose(a, b_, rtol=1e-12, atol=1e-15) and np.allclose(a, c_, rtol=1e-12, atol=1e-15)
+
+
+# ----------------------------------------------------------------------------- decode step
+def test_decode_step_is_append_prefill_with_one_token():
+    """A decode step is an append prefill with one appended token (Sec. 2.2,
+    decode phase): row i of a session with history M and N appended tokens is
+    the single row of a session with history M + i whose keys are the same
+    first M + i + 1 keys - for scores and for attention over the same ids."""
+    rng = np.random.default_rng(12)
+    M, N, H, d, ps = 300, 5, 2, 16, 16
+    q = rng.standard_normal((N, H, d)).astype(np.float32)
+    kI = rng.standard_normal((M + N, d)).astype(np.float32)
+    w = rng.random((N, H)).astype(np.float32)
+    pre = oracle.index_scores([0, N], [M], q, "f32", None, kI, "f32", None, w, np.arange(N), out_ld=M + N)
+    dec_hist = [M + i for i in range(N)]
+    dec_keys = np.concatenate([kI[:M + i + 1] for i in range(N)])
+    dec = oracle.index_scores(np.arange(N + 1), dec_hist, q, "f32", None, dec_keys, "f32", None, w, np.arange(N),
+                              out_ld=M + N)
+    assert np.array_equal(pre, dec)
+    # attention through one pool: every decode session maps its pages like the prefill session
+    Hq, dqk = 4, 32
+    pages = (M + N + ps - 1) // ps
+    pool = to_bf16_bits(rng.standard_normal((pages * ps, dqk)).astype(np.float32))
+    pt = np.arange(pages, dtype=np.int32)[None, :]
+    qa = to_bf16_bits(rng.standard_normal((N, Hq, dqk)).astype(np.float32))
+    sel = np.stack([rng.choice(M + i + 1, 40, replace=False) for i in range(N)]).astype(np.int32)
+    o1, l1 = oracle.sparse_attn([0, N], [M], np.arange(N), qa, pool, None, dqk, dqk, pt, ps, sel, 0.2, dqk)
+    o2, l2 = oracle.sparse_attn(np.arange(N + 1), dec_hist, np.arange(N), qa, pool, None, dqk, dqk,
+                                np.repeat(pt, N, axis=0), ps, sel, 0.2, dqk)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)

@@ -17,4 +17,6 @@ from .gen import (  # noqa: F401
     to_bf16_bits,
     quantize_fp8_per_row,
     synth_topk,
+    decode_lengths,
+    resident_pages,
 )

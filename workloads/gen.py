@@ -15,7 +15,7 @@ of rows can be regenerated without the rest:
     1 hot spans, 2 history indexer keys, 3 new-token indexer keys,
     4 indexer queries, 5 indexer head weights, 6 prediction noise,
     7 attention queries, 8 KV rows, 9 page table, 10 session lengths,
-    11 synthetic selections.
+    11 synthetic selections, 12 resident-page bitmaps.
 
 "Hot spans" stand in for concentrated relevance: 5% of each session's history
 sits in 8 contiguous spans whose indexer keys are multiplied by 3 before
@@ -35,7 +35,7 @@ from typing import Optional
 import numpy as np
 import torch
 
-S_HOT, S_KHIST, S_KNEW, S_Q, S_W, S_QNOISE, S_QATT, S_KV, S_PT, S_SESS, S_SEL = range(1, 12)
+S_HOT, S_KHIST, S_KNEW, S_Q, S_W, S_QNOISE, S_QATT, S_KV, S_PT, S_SESS, S_SEL, S_RES = range(1, 13)
 
 FP8_MAX = 448.0
 ATTN_Q_CHUNK = 64
@@ -46,6 +46,7 @@ CONFIG_NAMES = {
     2: "dsv32-layer-M131072-N8192-permuted",
     3: "ragged-16-sessions-M8K-64K",
     4: "prediction-8-layers-M131072-N4096",
+    5: "decode-16-sessions-M8K-48K-N1",
 }
 
 
@@ -288,7 +289,31 @@ def config(i: int, layer: int = 0, with_pred: Optional[bool] = None) -> Workload
                              seed=4, layer=layer, w_scale=1.0 / 8, table="identity", attn=MLA_ATTN,
                              q_pred_corr=0.9 if with_pred is None else (0.9 if with_pred else None),
                              name=CONFIG_NAMES[4])
+    if i == 5:
+        # decode: one appended token per session (the step of the decode
+        # phase), many sessions batched
+        rng = _rng(5, S_SESS)
+        M = np.floor(np.exp(rng.uniform(math.log(8192), math.log(49152), size=16))).astype(np.int32)
+        return make_workload(hist_len=M, new_len=np.ones(16, np.int32), H=64, d=128, idx_dtype="fp8", k=2048,
+                             seed=5, layer=layer, w_scale=1.0 / 8, table="permuted", attn=MLA_ATTN,
+                             name=CONFIG_NAMES[5])
     raise ValueError(i)
+
+
+def decode_lengths(B: int, lo: int, hi: int, seed: int) -> np.ndarray:
+    """History lengths of a batch of decoding sessions, log-uniform in [lo, hi]."""
+    rng = _rng(seed, S_SESS)
+    return np.floor(np.exp(rng.uniform(math.log(lo), math.log(hi), size=B))).astype(np.int32)
+
+
+def resident_pages(wl: Workload, p: float = 0.9, seed: int = 0) -> np.ndarray:
+    """A bitmap of pages already in HBM (bit j%32 of word j/32, LSB first):
+    each physical page independently with probability p."""
+    rng = _rng(wl.seed, S_RES, wl.layer, seed)
+    bits = rng.random(wl.num_phys_pages) < p
+    words = np.zeros((wl.num_phys_pages + 31) // 32 * 32, dtype=np.uint8)
+    words[:wl.num_phys_pages] = bits
+    return np.packbits(words.reshape(-1, 8), axis=1, bitorder="little").reshape(-1).view(np.uint32).copy()
 
 
 def attention_q_rows(wl: Workload, rows) -> np.ndarray:
