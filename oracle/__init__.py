@@ -48,6 +48,11 @@ def lib():
         L.jo_bf16_value.argtypes = [ctypes.c_uint16]
         L.jo_bf16_value.restype = dbl
         L.jo_index_scores.argtypes = [i32, P, P, P, i32, P, P, i32, P, P, i32, i32, i32, P, P, i64]
+        L.jo_index_scores_mxfp4.argtypes = [i32, P, P, P, i32, P, P, P, P, P, i32, i32, i32, P, P, i64]
+        L.jo_e2m1_value.argtypes = [ctypes.c_uint8]
+        L.jo_e2m1_value.restype = dbl
+        L.jo_e8m0_value.argtypes = [ctypes.c_uint8]
+        L.jo_e8m0_value.restype = dbl
         L.jo_topk.argtypes = [i32, P, P, i32, P, P, i64, i32, P]
         L.jo_topk_sharded.argtypes = [i32, P, P, i32, P, P, i64, i32, i32, i32, P]
         L.jo_page_demand.argtypes = [i32, P, P, P, i32, P, i32, i32, P, i32, P, P, P]
@@ -77,6 +82,32 @@ def _check(rc, what):
 
 def fp8_value(b: int) -> float:
     return lib().jo_fp8_e4m3fn_value(int(b))
+
+
+def e2m1_value(code: int) -> float:
+    return lib().jo_e2m1_value(int(code))
+
+
+def e8m0_value(e: int) -> float:
+    return lib().jo_e8m0_value(int(e))
+
+
+def index_scores_mxfp4(q_start, hist_len, q, q_dt, q_scale, kI, k_bscale, k_scale, w, rows, out_ld=None):
+    """Scores (float64) with MXFP4 indexer keys: kI [ctx rows, d/2] bytes,
+    k_bscale [ctx rows, d/32] E8M0 bytes."""
+    q_start = _c(q_start, np.int32)
+    hist_len = _c(hist_len, np.int32)
+    rows = _c(rows, np.int32)
+    H, d = q.shape[1], q.shape[2]
+    if out_ld is None:
+        out_ld = int((hist_len + np.diff(q_start)).max())
+    out = np.empty((rows.shape[0], out_ld), dtype=np.float64)
+    rc = lib().jo_index_scores_mxfp4(len(hist_len), _p(q_start), _p(hist_len), _p(np.ascontiguousarray(q)), DT[q_dt],
+                                     _p(_c(q_scale, np.float32)), _p(_c(kI, np.uint8)), _p(_c(k_bscale, np.uint8)),
+                                     _p(_c(k_scale, np.float32)), _p(_c(w, np.float32)), H, d, rows.shape[0],
+                                     _p(rows), _p(out), out_ld)
+    _check(rc, "index_scores_mxfp4")
+    return out
 
 
 def bf16_value(b: int) -> float:

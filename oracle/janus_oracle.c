@@ -23,6 +23,11 @@
  *     as defined under "Model-aligned prediction distance".
  *   - synchronization-free parallel prediction over history shards: Eq. (3),
  *     same section.
+ *   - FP4 indexer keys (Sec. "Experiments", models: DeepSeek-V4 keeps its
+ *     indexer keys in FP4), read as OCP MXFP4: e2m1 elements with one E8M0
+ *     scale per 32 elements.
+ *   - the decode phase as an append prefill with one appended token
+ *     (Sec. "Decode phase"): the same functions with one row per session.
  *   - read packing: maximal runs of selected, physically adjacent blocks,
  *     address-ordered, never including unselected blocks: Sec. "Best-effort
  *     read packing".  Runs are additionally split from their low end into
@@ -101,11 +106,70 @@ static int64_t key_base(const int32_t *q_start, const int32_t *hist_len, int b)
  * out[r * out_ld + s] for s < out_ld: the score of candidate s, -inf beyond
  * the causal limit M_b + i (and beyond the session's context).
  */
+/*
+ * OCP MX FP4 (e2m1): sign, two exponent bits (bias 1), one mantissa bit; an
+ * exponent field of 0 is the subnormal m * 2^-1.  No infinities or NaN.
+ */
+double jo_e2m1_value(uint8_t code)
+{
+    const int s = (code >> 3) & 1, e = (code >> 1) & 3, m = code & 1;
+    const double v = e == 0 ? 0.5 * m : (1.0 + 0.5 * m) * ldexp(1.0, e - 1);
+    return s ? -v : v;
+}
+
+/* OCP MX E8M0 shared scale: 2^(e - 127); 255 is NaN. */
+double jo_e8m0_value(uint8_t e)
+{
+    return e == 255 ? NAN : ldexp(1.0, (int)e - 127);
+}
+
+/*
+ * Element j of key row `row` in MXFP4 (DeepSeek-V4 stores indexer keys in
+ * FP4; read as OCP MXFP4): d/2 bytes per key, element j in the low nibble of
+ * byte j/2 when j is even and the high nibble when odd, times the E8M0 scale
+ * of its 32-element block (d/32 scale bytes per key).
+ */
+static double mxfp4_elem(const uint8_t *k, const uint8_t *bscale, int64_t row, int d, int j)
+{
+    const uint8_t byte = k[row * (d / 2) + j / 2];
+    const uint8_t code = (j & 1) ? (uint8_t)(byte >> 4) : (uint8_t)(byte & 15);
+    return jo_e2m1_value(code) * jo_e8m0_value(bscale[row * (d / 32) + j / 32]);
+}
+
+static int index_scores_impl(int nseq, const int32_t *q_start, const int32_t *hist_len,
+                             const void *q, int q_dt, const float *q_scale,
+                             const void *kI, int k_dt, const uint8_t *k_bscale, const float *k_scale,
+                             const float *w, int H, int d,
+                             int nrows, const int32_t *rows, double *out, int64_t out_ld);
+
 int jo_index_scores(int nseq, const int32_t *q_start, const int32_t *hist_len,
                     const void *q, int q_dt, const float *q_scale,
                     const void *kI, int k_dt, const float *k_scale,
                     const float *w, int H, int d,
                     int nrows, const int32_t *rows, double *out, int64_t out_ld)
+{
+    return index_scores_impl(nseq, q_start, hist_len, q, q_dt, q_scale, kI, k_dt, NULL, k_scale, w, H, d, nrows,
+                             rows, out, out_ld);
+}
+
+/* Eq. 1's scores with MXFP4 indexer keys (kI: [ctx rows][d/2] bytes, k_bscale: [ctx rows][d/32] E8M0). */
+int jo_index_scores_mxfp4(int nseq, const int32_t *q_start, const int32_t *hist_len,
+                          const void *q, int q_dt, const float *q_scale,
+                          const uint8_t *kI, const uint8_t *k_bscale, const float *k_scale,
+                          const float *w, int H, int d,
+                          int nrows, const int32_t *rows, double *out, int64_t out_ld)
+{
+    if (!k_bscale || d % 32 != 0)
+        return -1;
+    return index_scores_impl(nseq, q_start, hist_len, q, q_dt, q_scale, kI, -1, k_bscale, k_scale, w, H, d, nrows,
+                             rows, out, out_ld);
+}
+
+static int index_scores_impl(int nseq, const int32_t *q_start, const int32_t *hist_len,
+                             const void *q, int q_dt, const float *q_scale,
+                             const void *kI, int k_dt, const uint8_t *k_bscale, const float *k_scale,
+                             const float *w, int H, int d,
+                             int nrows, const int32_t *rows, double *out, int64_t out_ld)
 {
     if (nseq < 1 || H < 1 || d < 1 || nrows < 0)
         return -1;
@@ -133,7 +197,8 @@ int jo_index_scores(int nseq, const int32_t *q_start, const int32_t *hist_len,
                 continue;
             }
             for (int j = 0; j < d; j++)
-                kd[j] = elem(kI, k_dt, (kb + s) * d + j);
+                kd[j] = k_bscale ? mxfp4_elem((const uint8_t *)kI, k_bscale, kb + s, d, j)
+                                 : elem(kI, k_dt, (kb + s) * d + j);
             double acc = 0.0;
             for (int h = 0; h < H; h++) {
                 double x = 0.0;

@@ -455,3 +455,67 @@ def test_decode_step_is_append_prefill_with_one_token():
     o2, l2 = oracle.sparse_attn(np.arange(N + 1), dec_hist, np.arange(N), qa, pool, None, dqk, dqk,
                                 np.repeat(pt, N, axis=0), ps, sel, 0.2, dqk)
     assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+
+
+# ----------------------------------------------------------------------------- MXFP4 indexer keys
+# OCP MX v1.0, FP4 (E2M1) element encodings: code -> value (sign in bit 3)
+OCP_E2M1 = {0b0000: 0.0, 0b0001: 0.5, 0b0010: 1.0, 0b0011: 1.5, 0b0100: 2.0, 0b0101: 3.0, 0b0110: 4.0, 0b0111: 6.0}
+
+
+def test_e2m1_and_e8m0_tables():
+    for c, v in OCP_E2M1.items():
+        assert oracle.e2m1_value(c) == v and oracle.e2m1_value(c | 8) == -v
+    assert math.copysign(1.0, oracle.e2m1_value(8)) == -1.0  # negative zero
+    assert oracle.e8m0_value(127) == 1.0 and oracle.e8m0_value(130) == 8.0 and oracle.e8m0_value(120) == 2.0 ** -7
+    assert oracle.e8m0_value(0) == 2.0 ** -127 and oracle.e8m0_value(254) == 2.0 ** 127
+    assert math.isnan(oracle.e8m0_value(255))
+
+
+def _decode_mxfp4_table(packed, E):
+    """MXFP4 keys to float32 through the OCP table (exact: e2m1 x 2^k)."""
+    n, half = packed.shape
+    codes = np.empty((n, 2 * half), np.uint8)
+    codes[:, 0::2], codes[:, 1::2] = packed & 15, packed >> 4
+    mag = np.array([OCP_E2M1[c & 7] for c in range(16)])[codes]
+    val = np.where(codes & 8, -mag, mag) * np.repeat(np.exp2(E.astype(np.float64) - 127), 32, axis=1)
+    return val.astype(np.float32)
+
+
+@pytest.mark.parametrize("H,d", [(2, 64), (4, 128)])
+def test_mxfp4_scores_are_the_f32_scores_of_the_decoded_keys(H, d):
+    """The MXFP4 path equals the (separately pinned) f32 path fed the decoded
+    key values, bit for bit; queries are fp8 with per-token scales in both."""
+    from workloads import quantize_mxfp4
+    rng = np.random.default_rng(H + d)
+    hist, new = [300, 90], [4, 3]
+    ctx = sum(hist) + sum(new)
+    kf = (rng.standard_normal((ctx, d)) * rng.choice([0.01, 1.0, 50.0], size=(ctx, 1))).astype(np.float32)
+    packed, E = quantize_mxfp4(kf)
+    from workloads import quantize_fp8_per_row
+    q, qs = quantize_fp8_per_row(rng.standard_normal((sum(new), H, d)).astype(np.float32))
+    w = rng.random((sum(new), H)).astype(np.float32)
+    ks = rng.uniform(0.5, 2.0, ctx).astype(np.float32)
+    qst = np.array([0, new[0], sum(new)])
+    rows = np.arange(sum(new))
+    got = oracle.index_scores_mxfp4(qst, hist, q, "fp8", qs, packed, E, ks, w, rows)
+    ref = oracle.index_scores(qst, hist, q, "fp8", qs, _decode_mxfp4_table(packed, E), "f32", ks, w, rows)
+    assert np.array_equal(got, ref)
+
+
+def test_mxfp4_constant_keys_closed_form():
+    """Every key element = code 0b0010 (1.0) at block scale 2^3: k = 8 * ones,
+    so S[t,s] = sq[t] * sum_h w[t,h] * max(0, 8 * sum_j q[t,h,j])."""
+    rng = np.random.default_rng(31)
+    H, d, M, N = 3, 64, 50, 2
+    packed = np.full((M + N, d // 2), 0x22, np.uint8)
+    E = np.full((M + N, d // 32), 130, np.uint8)
+    q = rng.standard_normal((N, H, d)).astype(np.float32)
+    from workloads import quantize_fp8_per_row
+    q8, qs = quantize_fp8_per_row(q)
+    w = rng.random((N, H)).astype(np.float32)
+    got = oracle.index_scores_mxfp4([0, N], [M], q8, "fp8", qs, packed, E, None, w, np.arange(N))
+    qd = np.array([oracle.fp8_value(b) for b in q8.reshape(-1)]).reshape(N, H, d)
+    for t in range(N):
+        want = qs[t] * (w[t] * np.maximum(0.0, 8.0 * qd[t].sum(axis=1))).sum()
+        assert np.allclose(got[t, :M + t + 1], want, rtol=1e-12, atol=0)
+        assert np.all(np.isneginf(got[t, M + t + 1:]))

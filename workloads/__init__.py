@@ -16,6 +16,8 @@ from .gen import (  # noqa: F401
     to_fp8_bytes,
     to_bf16_bits,
     quantize_fp8_per_row,
+    quantize_mxfp4,
+    E2M1_MAGNITUDES,
     synth_topk,
     decode_lengths,
     resident_pages,

@@ -75,6 +75,33 @@ def quantize_fp8_per_row(x: np.ndarray):
     return q, scale
 
 
+# OCP MX FP4 (e2m1) element magnitudes by code 0..7 (the sign is bit 3)
+E2M1_MAGNITUDES = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def quantize_mxfp4(x: np.ndarray):
+    """float32 [n, d] -> (bytes [n, d/2], E8M0 scales [n, d/32]) in OCP MXFP4.
+
+    Per 32-element block the shared exponent is ceil(log2(amax / 6)), the
+    smallest that fits the block's largest magnitude within the e2m1 maximum
+    of 6, stored as E8M0 (biased by 127, clamped to [0, 254]); elements are
+    divided by 2^exponent, rounded to the nearest e2m1 value (ties to the
+    even code) and clamped to +-6.  Element j sits in the
+    low nibble of byte j/2 when j is even, the high nibble when odd."""
+    n, d = x.shape
+    blk = x.astype(np.float64).reshape(n, d // 32, 32)
+    amax = np.abs(blk).max(axis=2)
+    e = np.where(amax > 0, np.ceil(np.log2(np.where(amax > 0, amax, 6.0) / 6.0)), 0)
+    E = np.clip(e + 127, 0, 254).astype(np.uint8)
+    v = blk / np.exp2(E.astype(np.float64) - 127)[:, :, None]
+    mag = np.minimum(np.abs(v), 6.0)
+    dist = np.abs(mag[..., None] - E2M1_MAGNITUDES) + (np.arange(8) & 1) * 1e-300
+    code = np.argmin(dist, axis=-1).astype(np.uint8) | np.where(v < 0, 8, 0).astype(np.uint8)
+    code = code.reshape(n, d)
+    packed = (code[:, 0::2] | (code[:, 1::2] << 4)).astype(np.uint8)
+    return packed, E
+
+
 def _encode(x: np.ndarray, dtype: str):
     if dtype == "fp8":
         return quantize_fp8_per_row(x)
@@ -128,6 +155,7 @@ class Workload:
     attn_cfg: dict = field(default_factory=dict)
     q_pred: Optional[np.ndarray] = None
     q_pred_scale: Optional[np.ndarray] = None
+    k_bscale: Optional[np.ndarray] = None   # MXFP4 keys: E8M0 [total_ctx, d/32]; kI is then [total_ctx, d/2]
 
     # ---- derived batch description -------------------------------------
     @property
@@ -190,7 +218,7 @@ def _hot_spans(rng: np.random.Generator, M: int, n_spans: int = 8, frac: float =
 
 def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_run=32,
                   seed=0, layer=0, w_scale=1.0, hot=True, table="identity",
-                  attn=None, q_pred_corr=None, name="custom") -> Workload:
+                  attn=None, q_pred_corr=None, name="custom", key_format=None) -> Workload:
     """Build one layer's indexer inputs for a (possibly ragged) batch of sessions.
 
     ``table`` is "identity" (logical page p of session b -> physical page
@@ -228,7 +256,12 @@ def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_ru
     w = (_rng(seed, S_W, layer).random((total_q, H), dtype=np.float32) * np.float32(w_scale)).astype(np.float32)
 
     q, q_scale = _encode(q_f, idx_dtype)
-    kI, k_scale = _encode(kI_f, idx_dtype)
+    k_bscale = None
+    if key_format == "mxfp4":  # FP4 indexer keys with per-32 E8M0 scales (no per-token scale)
+        kI, k_bscale = quantize_mxfp4(kI_f)
+        k_scale = None
+    else:
+        kI, k_scale = _encode(kI_f, idx_dtype)
 
     q_pred = q_pred_scale = None
     if q_pred_corr is not None:
@@ -257,7 +290,7 @@ def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_ru
                     H=H, d=d, idx_dtype=idx_dtype, q=q, q_scale=q_scale, kI=kI, k_scale=k_scale,
                     w=w, k=k, page_size=page_size, max_run=max_run, page_table=pt,
                     num_phys_pages=num_phys, hot_spans=spans, attn_cfg=dict(attn or {}),
-                    q_pred=q_pred, q_pred_scale=q_pred_scale)
+                    q_pred=q_pred, q_pred_scale=q_pred_scale, k_bscale=k_bscale)
 
 
 MLA_ATTN = dict(Hq=128, dqk=576, dv=512, mla=True, q_std=1.0, kv_std=1.0 / math.sqrt(576.0),
