@@ -5,6 +5,7 @@
  * One append prefill of a layer, for a batch of sessions, is
  *
  *   janus_index_scores  indexer relevance of every candidate token   (Eq. 1)
+ *   janus_index_scores_mxfp4  the same with MXFP4 (FP4) indexer keys
  *   janus_topk          the k best candidates per appended token     (Eq. 1)
  *   janus_topk_sharded  per-shard top-(k/G) over G history shards    (Eq. 3)
  *   janus_page_demand   union of the selections as a page set, plus
@@ -112,6 +113,28 @@ int janus_index_scores(const janus_batch *b,
                        const void *kI, janus_dtype k_dt, const float *k_scale,
                        const float *w, int H, int d,
                        float *scores, void *stream);
+
+/*
+ * The same scores with MXFP4 indexer keys (DeepSeek-V4 keeps its indexer
+ * keys in FP4; Sec. 5.1, models), read as OCP MXFP4: each key is d/2 bytes of
+ * e2m1 elements (element j in the low nibble of byte j/2 when j is even, the
+ * high nibble when odd) and d/32 E8M0 scale bytes, one per 32 elements,
+ * element value = e2m1 * 2^(E - 127).
+ *   q              device [total_q, H, d] fp8 e4m3fn, q_scale [total_q] or NULL
+ *   kI             device [total_ctx, d/2] bytes
+ *   k_block_scale  device [total_ctx, d/32] E8M0 bytes
+ *   k_scale        device [total_ctx] fp32 or NULL (a per-token factor on top)
+ *   w, scores      as for janus_index_scores
+ * Products run on the fp8 x fp4 block-scaled MFMA; each head's product is
+ * rounded to bf16 and the head weights are applied in bf16 (relative error
+ * <= 2^-8 per term).  Requires H = 64, d = 128 and contexts up to 2^24 tokens
+ * (else JANUS_ERR_UNSUPPORTED; d not a multiple of 32: JANUS_ERR_INVALID_ARG).
+ */
+int janus_index_scores_mxfp4(const janus_batch *b,
+                             const void *q, const float *q_scale,
+                             const void *kI, const uint8_t *k_block_scale,
+                             const float *k_scale, const float *w, int H, int d,
+                             float *scores, void *stream);
 
 /*
  * Top-k per appended token (the selection of Eq. 1): the k largest scores of

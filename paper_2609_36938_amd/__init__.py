@@ -60,10 +60,11 @@ def lib():
         L.janus_predict_diff.argtypes = [P, P, i32, i32, P, P, P, P]
         L.janus_sparse_attn.argtypes = [BP, P, i32, i32, i32, P, P, i64, i64, P, i32, i32, P, i32, f32, P, i32,
                                         P, P]
+        L.janus_index_scores_mxfp4.argtypes = [BP, P, P, P, P, P, P, i32, i32, P, P]
         L.janus_sparse_attn_split.argtypes = [BP, P, i32, i32, i32, P, P, i64, i64, P, i32, i32, P, i32, f32, P,
                                               i32, P, i32, P, SZ, P]
         for f in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
-                  "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split"):
+                  "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split", "janus_index_scores_mxfp4"):
             getattr(L, f).restype = ctypes.c_int
         L.janus_status_string.argtypes = [ctypes.c_int]
         L.janus_status_string.restype = ctypes.c_char_p
@@ -142,6 +143,19 @@ def index_scores(batch: Batch, q, kI, w, q_scale=None, k_scale=None, scores=None
     rc = lib().janus_index_scores(batch.ref, _ptr(q), qd, _ptr(q_scale), _ptr(kI), kd, _ptr(k_scale), _ptr(w), H, d,
                                   _ptr(scores), _stream(stream))
     _check(rc, "janus_index_scores")
+    return scores
+
+
+def index_scores_mxfp4(batch: Batch, q, kI, k_block_scale, w, q_scale=None, k_scale=None, scores=None, stream=None):
+    """janus_index_scores_mxfp4: q fp8 bytes [total_q, H, d]; kI MXFP4 bytes
+    [total_ctx, d/2] with E8M0 block scales [total_ctx, d/32]; returns the flat
+    fp32 score buffer laid out as for index_scores."""
+    H, d = int(q.shape[1]), int(q.shape[2])
+    if scores is None:
+        scores = torch.empty(batch.total_scores, dtype=torch.float32, device=q.device)
+    rc = lib().janus_index_scores_mxfp4(batch.ref, _ptr(q), _ptr(q_scale), _ptr(kI), _ptr(k_block_scale),
+                                        _ptr(k_scale), _ptr(w), H, d, _ptr(scores), _stream(stream))
+    _check(rc, "janus_index_scores_mxfp4")
     return scores
 
 

@@ -123,6 +123,85 @@ JANUS_DEV void head_group(float &acc, const v8i &a0, const v8i &a1, const v8i &a
             : IDX_HEAD_GROUP_CLOBBERS);
 }
 
+// The same group with MXFP4 keys, after expand_e2m1 has widened them to fp8
+// (sa = 2^6 undoes its 2^-6, sb is the lane's E8M0 block scale).  Block
+// scales can make a product of any size, so ReLU is not folded into the
+// convert here: each pair is rounded to bf16, its sign clamped with a packed
+// int16 max (a negative bf16 is a negative int16), and dotted with the
+// weights.  Convert, max and dot of a pair are at least two instructions apart
+// (one wait state after a VALU write read by a packed op).
+#define IDX_MFMA_F4(dst, a) \
+    "v_mfma_scale_f32_16x16x128_f8f6f4 " dst ", %[" a "], %[bk], 0, %[sa], %[sb] op_sel_hi:[0,0,0]\n\t"
+#define F4_CVT(r, r1) "v_cvt_pk_bf16_f32 v" #r ", v" #r ", v" #r1 "\n\t"
+#define F4_MAX(r) "v_pk_max_i16 v" #r ", v" #r ", 0\n\t"
+#define F4_DOT(r, w) "v_dot2c_f32_bf16 %[acc], v" #r ", %[" w "]\n\t"
+#define IDX_HEAD_GROUP_F4(INIT)                                                                          \
+    INIT "s_nop 1\n\t" IDX_MFMA_F4("v[112:115]", "a0") IDX_MFMA_F4("v[116:119]", "a1")                    \
+        IDX_MFMA_F4("v[120:123]", "a2") IDX_MFMA_F4("v[124:127]", "a3") "s_nop 11\n\t"                   \
+        F4_CVT(112, 113)                                                                                   \
+        F4_CVT(114, 115) F4_MAX(112)                                                                       \
+        F4_CVT(116, 117) F4_MAX(114) F4_DOT(112, "w00")                                                    \
+        F4_CVT(118, 119) F4_MAX(116) F4_DOT(114, "w01")                                                    \
+        F4_CVT(120, 121) F4_MAX(118) F4_DOT(116, "w10")                                                    \
+        F4_CVT(122, 123) F4_MAX(120) F4_DOT(118, "w11")                                                    \
+        F4_CVT(124, 125) F4_MAX(122) F4_DOT(120, "w20")                                                    \
+        F4_CVT(126, 127) F4_MAX(124) F4_DOT(122, "w21")                                                    \
+        F4_MAX(126) F4_DOT(124, "w30")                                                                     \
+        F4_DOT(126, "w31") "s_nop 2"
+#define IDX_HEAD_GROUP_F4_INPUTS                                                                       \
+    [a0] "v"(a0), [a1] "v"(a1), [a2] "v"(a2), [a3] "v"(a3), [bk] "v"(bk), [sa] "v"(sa), [sb] "v"(sb),   \
+        [w00] "v"(w[0][0]), [w01] "v"(w[0][1]), [w10] "v"(w[1][0]), [w11] "v"(w[1][1]), [w20] "v"(w[2][0]), \
+        [w21] "v"(w[2][1]), [w30] "v"(w[3][0]), [w31] "v"(w[3][1])
+
+// MXFP4 keys as fp8: an e2m1 nibble (sign, 2-bit exponent, 1-bit mantissa,
+// bias 1) placed at bits 7 and 4..2 of a byte is the e4m3 code (bias 7) of
+// the same value times 2^-6; the e2m1 subnormal 0.5 lands on the e4m3
+// subnormal 2^-7, and zero on zero.  Of 8 nibbles (element 2i in the low
+// nibble of byte i) the low nibbles give elements 0, 2, 4, 6 and the high
+// ones 1, 3, 5, 7: the query operand is put in the same order by evens_odds,
+// which leaves every dot product as it was.
+JANUS_DEV v8i expand_e2m1(const v4i &u)
+{
+    v8i r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const uint32_t x = (uint32_t)u[i];
+        r[2 * i] = (int)(((x << 4) & 0x80808080u) | ((x << 2) & 0x1C1C1C1Cu));
+        r[2 * i + 1] = (int)((x & 0x80808080u) | ((x >> 2) & 0x1C1C1C1Cu));
+    }
+    return r;
+}
+
+// fp8 elements 8i .. 8i+7 (registers 2i, 2i+1) -> the even ones in register
+// 2i, the odd ones in 2i+1
+JANUS_DEV v8i evens_odds(const v8i &a)
+{
+    v8i r;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        r[2 * i] = (int)__builtin_amdgcn_perm((uint32_t)a[2 * i + 1], (uint32_t)a[2 * i], 0x06040200u);
+        r[2 * i + 1] = (int)__builtin_amdgcn_perm((uint32_t)a[2 * i + 1], (uint32_t)a[2 * i], 0x07050301u);
+    }
+    return r;
+}
+constexpr int F4_QUERY_SCALE = 127 + 6;  // E8M0 2^6
+
+template <bool FIRST>
+JANUS_DEV void head_group_f4(float &acc, const v8i &a0, const v8i &a1, const v8i &a2, const v8i &a3, const v8i &bk,
+                             int sa, int sb, const v2bf (*w)[2])
+{
+    if (FIRST)
+        asm(IDX_HEAD_GROUP_F4("v_mov_b32 %[acc], 0\n\t")
+            : [acc] "=&v"(acc)
+            : IDX_HEAD_GROUP_F4_INPUTS
+            : IDX_HEAD_GROUP_CLOBBERS);
+    else
+        asm(IDX_HEAD_GROUP_F4("")
+            : [acc] "+v"(acc)
+            : IDX_HEAD_GROUP_F4_INPUTS
+            : IDX_HEAD_GROUP_CLOBBERS);
+}
+
 constexpr int IDX_STAGE = 128;                      // keys per LDS stage (16 KB)
 constexpr int IDX_XCD = 8;                          // L2 domains (XCDs) of the chip
 
@@ -410,74 +489,112 @@ __global__ __launch_bounds__(256) void index_scores_vector(
 
 namespace janus {
 
-// Decode-shaped batches (every session appends at most DEC_MAXQ tokens, as in
-// the decode phase): the scores are a GEMV over each session's keys, bound
-// by reading the keys once.  Block (key chunk c, session b): the four waves
-// take the chunk's 64-key groups in turn; a wave reads a group's keys (and
-// their scales) straight from global memory one group ahead - each key is
-// used by this block alone, so nothing is staged in LDS - and for every
-// token runs one head group per 16-key block: four 16x16x128 MFMAs (16 heads
-// x 16 keys each) with the clamped-bf16 epilogue of the prefill kernel.  Lane
-// group g then stores 16-key block g of the group: one 256-byte store per
-// token and group.
-constexpr int DEC_MAXQ = 4;
-constexpr int DEC_CHUNK = 4096;   // keys per block
+// Row-tile kernel: a block takes up to NQ tokens of one session and one
+// 4096-key chunk.  It serves decode-shaped batches (every session appends at
+// most NQ tokens, as in the decode phase: the scores are a GEMV over each
+// session's keys, bound by reading the keys once) and MXFP4 keys at any size.
+// The four waves take the chunk's 64-key groups in turn; a wave reads a
+// group's keys (and their scales) straight from global memory one group ahead
+// - each key is used by this block alone, so nothing is staged in LDS - and
+// for every token runs one head group per 16-key block: four 16x16x128 MFMAs
+// (16 heads x 16 keys each) and the epilogue.  Lane group g then stores
+// 16-key block g of the group: one 256-byte store per token and group.
+// Groups wholly past every token's causal limit skip the MFMAs (their stores
+// write -inf).
+constexpr int ROWS_NQ = 4;
+constexpr int ROWS_CHUNK = 4096;   // keys per block
 
-template <int NQ>
-__global__ __launch_bounds__(256, 2) void index_scores_fp8_decode(
+template <int NQ, bool FP4>
+__global__ __launch_bounds__(256, 2) void index_scores_rows(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
-    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start,
-    const uint8_t *__restrict__ q, const float *__restrict__ q_scale, const uint8_t *__restrict__ kI,
-    const float *__restrict__ k_scale, const float *__restrict__ w, float *__restrict__ scores)
+    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs, int nchunks,
+    int one_tile, const uint8_t *__restrict__ q, const float *__restrict__ q_scale, const uint8_t *__restrict__ kI,
+    const uint8_t *__restrict__ k_bscale, const float *__restrict__ k_scale, const float *__restrict__ w,
+    float *__restrict__ scores)
 {
-    const int b = blockIdx.y;
+    // block = (tile, chunk), chunk fastest; with one tile per session the
+    // tile is the session
+    const int tile = blockIdx.x / nchunks;
+    const int c0 = (blockIdx.x - tile * nchunks) * ROWS_CHUNK;
+    int b = tile, t0 = 0;
+    if (!one_tile && !tile_slot(q_start, num_seqs, tile, NQ, b, t0))
+        return;
     const int qs = q_start[b], N = q_start[b + 1] - qs;
     const int M = hist_len[b], ctx = M + N;
-    const int c0 = blockIdx.x * DEC_CHUNK;
-    if (N == 0 || c0 >= ctx)
+    const int nv = min(NQ, N - t0);  // tokens of this tile
+    if (nv <= 0 || c0 >= ctx)
         return;
     const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int r16 = lane & 15, kg = lane >> 4;
     // A operand of token t, head tile hb: row r16 = head 16hb + r16, bytes
-    // 32kg .. 32kg+31; this lane's output rows 4kg .. 4kg+3 are heads
-    // 16hb + 4kg + i, whose weights (times the query scale and 2^25) it holds
+    // 32kg .. 32kg+31 (for MXFP4 keys reordered by evens_odds); this lane's
+    // output rows 4kg .. 4kg+3 are heads
+    // 16hb + 4kg + i, whose weights (times the query scale, and for fp8 keys
+    // times 2^25) it holds
     v8i a[NQ][4];
     v2bf wv[NQ][4][2];
+    // MXFP4: the scaled MFMA takes K 16kg .. 16kg+15 from this lane's low 16
+    // bytes, K 64+16kg .. from its high 16, and the E8M0 scale of K block b
+    // (32 elements) from lane group b.  Lane group kg therefore holds half kg%2
+    // of MX blocks kg/2 and 2+kg/2, so each hardware block is one MX block,
+    // the one whose scale this lane supplies.
+    const int f4_half = 32 * (kg >> 1) + 16 * (kg & 1);  // first element of the low half
 #pragma unroll
     for (int t = 0; t < NQ; ++t) {
-        const bool ok = t < N;
-        const int64_t row = qs + (ok ? t : 0);
-        const float sq = (q_scale ? q_scale[row] : 1.0f) * 0x1p25f;
+        const bool ok = t < nv;
+        const int64_t row = qs + t0 + (ok ? t : 0);
+        const float sq = (q_scale ? q_scale[row] : 1.0f) * (FP4 ? 1.0f : 0x1p25f);
 #pragma unroll
         for (int hb = 0; hb < 4; ++hb) {
-            a[t][hb] = ok ? *(const v8i *)(q + ((row * 64 + 16 * hb + r16) << 7) + 32 * kg)
-                          : v8i{0, 0, 0, 0, 0, 0, 0, 0};
+            const uint8_t *qr = q + ((row * 64 + 16 * hb + r16) << 7);
+            if constexpr (FP4) {
+                const v4i lo = ok ? *(const v4i *)(qr + f4_half) : v4i{0, 0, 0, 0};
+                const v4i hi = ok ? *(const v4i *)(qr + 64 + f4_half) : v4i{0, 0, 0, 0};
+                a[t][hb] = evens_odds(v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+            } else {
+                a[t][hb] = ok ? *(const v8i *)(qr + 32 * kg) : v8i{0, 0, 0, 0, 0, 0, 0, 0};
+            }
             const v4f tw = *(const v4f *)(w + row * 64 + 16 * hb + 4 * kg);
             wv[t][hb][0] = __builtin_convertvector((v2f){tw[0] * sq, tw[1] * sq}, v2bf);
             wv[t][hb][1] = __builtin_convertvector((v2f){tw[2] * sq, tw[3] * sq}, v2bf);
         }
     }
-    const int scales = IDX_MFMA_SCALES;
-    // the session's keys (and key scales) from c0 on: rows past the context
-    // read as zeros; its score rows (row t at t * ctx): stores past them drop
+    constexpr int KB = FP4 ? 64 : 128;  // key bytes
+    // the session's keys (block scales, key scales) from c0 on: rows past the
+    // context read as zeros; its score rows (row t at t * ctx): stores past
+    // them drop
     const int64_t kbase = (int64_t)ctx_start[b] + c0;
-    const __amdgpu_buffer_rsrc_t krs = make_buffer_rsrc((void *)(kI + (kbase << 7)), (uint32_t)(ctx - c0) << 7);
+    const __amdgpu_buffer_rsrc_t krs = make_buffer_rsrc((void *)(kI + kbase * KB), (uint32_t)(ctx - c0) * KB);
+    const __amdgpu_buffer_rsrc_t bsr =
+        make_buffer_rsrc((void *)(FP4 ? k_bscale + kbase * 4 : nullptr), FP4 ? (uint32_t)(ctx - c0) * 4u : 0u);
     const __amdgpu_buffer_rsrc_t ksr =
         make_buffer_rsrc((void *)(k_scale ? k_scale + kbase : nullptr), k_scale ? (uint32_t)(ctx - c0) << 2 : 0u);
-    const __amdgpu_buffer_rsrc_t srs = make_buffer_rsrc(scores + score_start[b], (uint32_t)(N * ctx) << 2);
-    const int ngroups = (min(DEC_CHUNK, ctx - c0) + 63) / 64;
+    const __amdgpu_buffer_rsrc_t srs =
+        make_buffer_rsrc(scores + score_start[b] + (int64_t)t0 * ctx, (uint32_t)(nv * ctx) << 2);
+    const int ngroups = (min(ROWS_CHUNK, ctx - c0) + 63) / 64;
+    const int last_lim = M + t0 + nv - 1;  // largest causal limit in the tile
 
     struct Group {
-        v4i k[8];   // 16-key block j: key row 16j + r16, bytes 32kg .. +31
+        v4i k[8];   // 16-key block j: key row 16j + r16; fp8: bytes 32kg.. in k[2j], k[2j+1]; fp4: both halves in k[j]
+        int bs[4];  // fp4: the E8M0 scales of key row 16j + r16, block kg in the low byte
         float ks;   // scale of key 16kg + r16 (the one this lane stores)
     };
     auto load = [&](int g, Group &G) {
-        const uint32_t off = (uint32_t)(64 * g + r16) * 128u + 32u * kg;
+        const uint32_t row0 = (uint32_t)(64 * g + r16);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            G.k[2 * j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(krs, off + 2048u * j, 0, 0));
-            G.k[2 * j + 1] =
-                __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(krs, off + 2048u * j + 16u, 0, 0));
+            const uint32_t row = row0 + 16u * j;
+            if constexpr (FP4) {
+                const v2i lo = __builtin_bit_cast(v2i, __builtin_amdgcn_raw_buffer_load_b64(krs, row * 64u + f4_half / 2, 0, 0));
+                const v2i hi =
+                    __builtin_bit_cast(v2i, __builtin_amdgcn_raw_buffer_load_b64(krs, row * 64u + 32u + f4_half / 2, 0, 0));
+                G.k[j] = v4i{lo[0], lo[1], hi[0], hi[1]};
+                G.bs[j] = (int)(__builtin_amdgcn_raw_buffer_load_b32(bsr, row * 4u, 0, 0) >> (8 * kg));
+            } else {
+                const uint32_t off = row0 * 128u + 32u * kg + 2048u * j;
+                G.k[2 * j] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(krs, off, 0, 0));
+                G.k[2 * j + 1] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(krs, off + 16u, 0, 0));
+            }
         }
         G.ks = k_scale ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
                                                        ksr, (uint32_t)(64 * g + 16 * kg + r16) * 4u, 0, 0))
@@ -485,29 +602,37 @@ __global__ __launch_bounds__(256, 2) void index_scores_fp8_decode(
     };
     auto compute = [&](int g, const Group &G) {
         float res[NQ][4];
+        // (fp8 serves decode only: a group past every limit is rare there)
+        const bool masked = FP4 && c0 + 64 * g > last_lim;  // block-uniform
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const v8i bk = v8i{G.k[2 * j][0], G.k[2 * j][1], G.k[2 * j][2], G.k[2 * j][3],
-                               G.k[2 * j + 1][0], G.k[2 * j + 1][1], G.k[2 * j + 1][2], G.k[2 * j + 1][3]};
+            const v8i bk = FP4 ? expand_e2m1(G.k[j])
+                               : v8i{G.k[2 * j][0], G.k[2 * j][1], G.k[2 * j][2], G.k[2 * j][3],
+                                     G.k[2 * j + 1][0], G.k[2 * j + 1][1], G.k[2 * j + 1][2], G.k[2 * j + 1][3]};
 #pragma unroll
             for (int t = 0; t < NQ; ++t) {
-                if (t >= N)  // block-uniform
+                // block-uniform; a masked group's stores write -inf, a
+                // missing token's none
+                if (t >= nv || masked)
                     continue;
                 float r;
-                head_group<true>(r, a[t][0], a[t][1], a[t][2], a[t][3], bk, scales, &wv[t][0]);
+                if constexpr (FP4)
+                    head_group_f4<true>(r, a[t][0], a[t][1], a[t][2], a[t][3], bk, F4_QUERY_SCALE, G.bs[j],
+                                        &wv[t][0]);
+                else
+                    head_group<true>(r, a[t][0], a[t][1], a[t][2], a[t][3], bk, IDX_MFMA_SCALES, &wv[t][0]);
                 r += xor_lanes16(r);
                 r += __shfl_xor(r, 32, 64);
                 res[t][j] = r;
             }
         }
-        const int sl = 64 * g + 16 * kg + r16;  // key (from c0) this lane stores
-        const int s = c0 + sl;
+        const int s = c0 + 64 * g + 16 * kg + r16;  // the key this lane stores
 #pragma unroll
         for (int t = 0; t < NQ; ++t) {
-            if (t >= N)
+            if (t >= nv)
                 continue;
             float v = kg == 0 ? res[t][0] : kg == 1 ? res[t][1] : kg == 2 ? res[t][2] : res[t][3];
-            v = s > M + t ? -INFINITY : v * G.ks;
+            v = s > M + t0 + t ? -INFINITY : v * G.ks;
             const uint32_t off = s < ctx ? (uint32_t)(t * ctx + s) * 4u : 0x80000000u;
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), srs, off, 0, 0);
         }
@@ -525,6 +650,44 @@ __global__ __launch_bounds__(256, 2) void index_scores_fp8_decode(
         load(g + 8, A);
         compute(g + 4, B);
     }
+}
+
+}  // namespace janus
+
+namespace janus {
+
+// Tiles of the row-tile kernel: one per session when no session appends
+// more than NQ tokens, else an upper bound (ceil(total_q / NQ) + sessions).
+static int64_t rows_tiles(const janus_batch *bt, int nq)
+{
+    return bt->max_q <= nq ? bt->num_seqs : ceil_div(bt->total_q, nq) + (int64_t)bt->num_seqs;
+}
+static int rows_nq(const janus_batch *bt) { return bt->max_q <= 1 ? 1 : bt->max_q <= 2 ? 2 : ROWS_NQ; }
+static bool rows_grid_ok(const janus_batch *bt)
+{
+    return rows_tiles(bt, rows_nq(bt)) * ceil_div(bt->max_ctx, ROWS_CHUNK) <= INT32_MAX;
+}
+
+// 1-D grid of the row-tile kernel: (tile, 4096-key chunk), chunk fastest
+template <bool FP4>
+static void launch_rows(const janus_batch *bt, const void *q, const float *q_scale, const void *kI,
+                        const uint8_t *k_bscale, const float *k_scale, const float *w, float *scores, hipStream_t st)
+{
+    const int nq = rows_nq(bt);
+    const int nchunks = ceil_div(bt->max_ctx, ROWS_CHUNK);
+    const int one_tile = bt->max_q <= nq;
+    const dim3 grid((unsigned)(rows_tiles(bt, nq) * nchunks));
+    auto go = [&](auto kern) {
+        hipLaunchKernelGGL(kern, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start, bt->hist_len, bt->score_start,
+                           bt->num_seqs, nchunks, one_tile, (const uint8_t *)q, q_scale, (const uint8_t *)kI,
+                           k_bscale, k_scale, w, scores);
+    };
+    if (nq == 1)
+        go(index_scores_rows<1, FP4>);
+    else if (nq == 2)
+        go(index_scores_rows<2, FP4>);
+    else
+        go(index_scores_rows<ROWS_NQ, FP4>);
 }
 
 }  // namespace janus
@@ -548,20 +711,10 @@ extern "C" int janus_index_scores(const janus_batch *bt, const void *q, janus_dt
     const int nseq = bt->num_seqs;
     // the MFMA kernel addresses a session's keys and a block's score rows
     // with 32-bit buffer offsets: contexts up to 2^24 tokens
-    if (q_dt == JANUS_FP8_E4M3 && d == 128 && H == 64 && bt->max_ctx <= (1 << 24) && bt->max_q <= DEC_MAXQ) {
+    if (q_dt == JANUS_FP8_E4M3 && d == 128 && H == 64 && bt->max_ctx <= (1 << 24) && bt->max_q <= ROWS_NQ &&
+        rows_grid_ok(bt)) {
         // decode-shaped: one block per (session, 4096-key chunk)
-        const dim3 grid(ceil_div(bt->max_ctx, DEC_CHUNK), nseq);
-        const auto *qq = (const uint8_t *)q;
-        const auto *kk = (const uint8_t *)kI;
-        if (bt->max_q == 1)
-            hipLaunchKernelGGL(index_scores_fp8_decode<1>, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start,
-                               bt->hist_len, bt->score_start, qq, q_scale, kk, k_scale, w, scores);
-        else if (bt->max_q == 2)
-            hipLaunchKernelGGL(index_scores_fp8_decode<2>, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start,
-                               bt->hist_len, bt->score_start, qq, q_scale, kk, k_scale, w, scores);
-        else
-            hipLaunchKernelGGL(index_scores_fp8_decode<4>, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start,
-                               bt->hist_len, bt->score_start, qq, q_scale, kk, k_scale, w, scores);
+        launch_rows<false>(bt, q, q_scale, kI, nullptr, k_scale, w, scores, st);
         return launch_status();
     }
     if (q_dt == JANUS_FP8_E4M3 && d == 128 && H == 64 && bt->max_ctx <= (1 << 24)) {
@@ -583,5 +736,21 @@ extern "C" int janus_index_scores(const janus_batch *bt, const void *q, janus_dt
     hipLaunchKernelGGL(index_scores_vector, grid, dim3(GEN_TOK_TILE * GEN_KEY_TILE), 0, st, bt->q_start,
                        bt->ctx_start, bt->hist_len, bt->score_start, nseq, q, (int)q_dt, q_scale, kI, (int)k_dt,
                        k_scale, w, H, d, scores);
+    return launch_status();
+}
+
+extern "C" int janus_index_scores_mxfp4(const janus_batch *bt, const void *q, const float *q_scale, const void *kI,
+                                        const uint8_t *k_block_scale, const float *k_scale, const float *w, int H,
+                                        int d, float *scores, void *stream)
+{
+    if (!batch_ok(bt) || !bt->ctx_start || !bt->score_start || !q || !kI || !k_block_scale || !w || !scores ||
+        H < 1 || d < 1 || d % 32 != 0)
+        return JANUS_ERR_INVALID_ARG;
+    // the row-tile kernel: 64 heads x 128 dims, 32-bit buffer offsets
+    if (H != 64 || d != 128 || bt->max_ctx > (1 << 24) || !rows_grid_ok(bt))
+        return JANUS_ERR_UNSUPPORTED;
+    if (bt->total_q == 0 || bt->max_ctx == 0)
+        return JANUS_OK;
+    launch_rows<true>(bt, q, q_scale, kI, k_block_scale, k_scale, w, scores, as_stream(stream));
     return launch_status();
 }

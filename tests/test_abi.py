@@ -23,13 +23,14 @@ def _ensure_lib():
 
 def declared_symbols():
     text = open(HEADER).read()
-    return sorted(set(re.findall(r"\b(janus_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(janus_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_five_calls():
     syms = declared_symbols()
     for s in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
-              "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split", "janus_status_string"):
+              "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split", "janus_index_scores_mxfp4",
+              "janus_status_string"):
         assert s in syms
 
 
@@ -102,6 +103,14 @@ def test_invalid_arguments_are_rejected_on_host(L):
                                8, ctypes.c_float(0.1), FAKE, 2, None, None) == 2
     assert L.janus_sparse_attn(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 500, 576, FAKE, 4, 64, FAKE,
                                8, ctypes.c_float(0.1), FAKE, 1, None, None) == 1
+
+
+def test_mxfp4_scores_rejections(L):
+    b = _batch()
+    assert L.janus_index_scores_mxfp4(ctypes.byref(b), FAKE, None, FAKE, None, None, FAKE, 64, 128, FAKE, None) == 1
+    assert L.janus_index_scores_mxfp4(ctypes.byref(b), FAKE, None, FAKE, FAKE, None, FAKE, 64, 100, FAKE, None) == 1
+    assert L.janus_index_scores_mxfp4(ctypes.byref(b), FAKE, None, FAKE, FAKE, None, FAKE, 32, 128, FAKE, None) == 2
+    assert L.janus_index_scores_mxfp4(ctypes.byref(b), FAKE, None, FAKE, FAKE, None, FAKE, 64, 64, FAKE, None) == 2
 
 
 def test_split_attention_workspace_and_rejections(L):
