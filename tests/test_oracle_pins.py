@@ -519,3 +519,20 @@ def test_mxfp4_constant_keys_closed_form():
         want = qs[t] * (w[t] * np.maximum(0.0, 8.0 * qd[t].sum(axis=1))).sum()
         assert np.allclose(got[t, :M + t + 1], want, rtol=1e-12, atol=0)
         assert np.all(np.isneginf(got[t, M + t + 1:]))
+
+
+def test_mxfp4_generator_rounding():
+    """The key generator's MXFP4 encoding (input bytes, not method
+    arithmetic): the block exponent is the smallest that fits amax within 6,
+    elements round to the nearest e2m1 value with ties to the even code, and
+    decoding through the OCP table returns every representable input as is."""
+    from workloads import quantize_mxfp4
+    x = np.zeros((2, 32), np.float32)
+    x[0, :9] = [0.75, 0.25, 1.25, 1.75, 2.5, 3.5, 5.0, 6.0, -0.75]
+    x[1, :4] = [12.0, -3.0, 1.0, 8.0]  # amax 12 -> exponent 1
+    packed, E = quantize_mxfp4(x)
+    assert E[0, 0] == 127 and E[1, 0] == 128
+    codes = [(packed[0, j // 2] >> (4 * (j % 2))) & 15 for j in range(9)]
+    assert codes == [0b0010, 0b0000, 0b0010, 0b0100, 0b0100, 0b0110, 0b0110, 0b0111, 0b1010]
+    dec = _decode_mxfp4_table(packed, E)
+    assert np.array_equal(dec[1, :4], x[1, :4])

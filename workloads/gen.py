@@ -95,8 +95,11 @@ def quantize_mxfp4(x: np.ndarray):
     E = np.clip(e + 127, 0, 254).astype(np.uint8)
     v = blk / np.exp2(E.astype(np.float64) - 127)[:, :, None]
     mag = np.minimum(np.abs(v), 6.0)
-    dist = np.abs(mag[..., None] - E2M1_MAGNITUDES) + (np.arange(8) & 1) * 1e-300
-    code = np.argmin(dist, axis=-1).astype(np.uint8) | np.where(v < 0, 8, 0).astype(np.uint8)
+    dist = np.abs(mag[..., None] - E2M1_MAGNITUDES)
+    nearest = dist == dist.min(axis=-1, keepdims=True)  # one code, or two on a tie
+    even_first = nearest & ((np.arange(8) & 1) == 0)
+    code = np.where(even_first.any(axis=-1), np.argmax(even_first, axis=-1), np.argmax(nearest, axis=-1))
+    code = code.astype(np.uint8) | np.where(v < 0, 8, 0).astype(np.uint8)
     code = code.reshape(n, d)
     packed = (code[:, 0::2] | (code[:, 1::2] << 4)).astype(np.uint8)
     return packed, E
