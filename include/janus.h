@@ -72,19 +72,36 @@ typedef enum {
  * has a cached history of M_b tokens and appends N_b tokens (the P and L of
  * the paper's notation table).  Host fields size grids; device arrays locate
  * rows.  All device arrays are int32 except score_start.
+ *
+ * Entry granularity (the selection unit of DeepSeek-V4, Sec. 2.1 footnote;
+ * the notation table applies to entries unchanged).  With entry_shift = e > 0
+ * every candidate is an entry: one cached row (indexer key, KV) standing for
+ * the E = 2^e consecutive tokens [E*j, E*j + E - 1], which exists once its
+ * last token does.  Then, everywhere below, ids are entry ids and
+ *   - session b holds C_b = (M_b + N_b) >> e entries (key rows, score row
+ *     length), of which the (M_b >> e) below the append are history (M_b
+ *     in the history ranges of topk_sharded and page_demand reads M_b >> e);
+ *   - appended token i (position M_b + i) has the candidates
+ *     0 .. ((M_b + i + 1) >> e) - 1, the entries complete at its position;
+ *   - ctx_start and score_start are prefix sums of C_b and N_b * C_b, and
+ *     max_ctx / total_ctx the max / sum of C_b;
+ *   - pages hold page_size entries.
+ * entry_shift = 0 is token granularity: C_b = M_b + N_b, candidates
+ * 0 .. M_b + i.  entry_shift must lie in [0, 16].
  */
 typedef struct {
     int32_t num_seqs;            /* B >= 1                                        */
     int32_t total_q;             /* host: sum_b N_b                               */
     int32_t max_q;               /* host: max_b N_b                               */
-    int32_t max_ctx;             /* host: max_b (M_b + N_b)                       */
-    int64_t total_ctx;           /* host: sum_b (M_b + N_b)                       */
+    int32_t max_ctx;             /* host: max_b C_b (tokens: M_b + N_b)           */
+    int64_t total_ctx;           /* host: sum_b C_b                               */
     const int32_t *q_start;      /* device [B+1]: prefix sums of N_b -> rows of
                                     q, w, topk_idx and attention q/out            */
-    const int32_t *ctx_start;    /* device [B+1]: prefix sums of M_b+N_b -> rows
+    const int32_t *ctx_start;    /* device [B+1]: prefix sums of C_b -> rows
                                     of the indexer keys and their scales          */
     const int32_t *hist_len;     /* device [B]: M_b                               */
-    const int64_t *score_start;  /* device [B+1]: prefix sums of N_b*(M_b+N_b)    */
+    const int64_t *score_start;  /* device [B+1]: prefix sums of N_b*C_b          */
+    int32_t entry_shift;         /* log2 tokens per entry; 0 = token granularity */
 } janus_batch;
 
 /*

@@ -47,18 +47,18 @@ def lib():
         L.jo_fp8_e4m3fn_value.restype = dbl
         L.jo_bf16_value.argtypes = [ctypes.c_uint16]
         L.jo_bf16_value.restype = dbl
-        L.jo_index_scores.argtypes = [i32, P, P, P, i32, P, P, i32, P, P, i32, i32, i32, P, P, i64]
-        L.jo_index_scores_mxfp4.argtypes = [i32, P, P, P, i32, P, P, P, P, P, i32, i32, i32, P, P, i64]
+        L.jo_index_scores.argtypes = [i32, P, P, i32, P, i32, P, P, i32, P, P, i32, i32, i32, P, P, i64]
+        L.jo_index_scores_mxfp4.argtypes = [i32, P, P, i32, P, i32, P, P, P, P, P, i32, i32, i32, P, P, i64]
         L.jo_e2m1_value.argtypes = [ctypes.c_uint8]
         L.jo_e2m1_value.restype = dbl
         L.jo_e8m0_value.argtypes = [ctypes.c_uint8]
         L.jo_e8m0_value.restype = dbl
-        L.jo_topk.argtypes = [i32, P, P, i32, P, P, i64, i32, P]
-        L.jo_topk_sharded.argtypes = [i32, P, P, i32, P, P, i64, i32, i32, i32, P]
-        L.jo_page_demand.argtypes = [i32, P, P, P, i32, P, i32, i32, P, i32, P, P, P]
+        L.jo_topk.argtypes = [i32, P, P, i32, i32, P, P, i64, i32, P]
+        L.jo_topk_sharded.argtypes = [i32, P, P, i32, i32, P, P, i64, i32, i32, i32, P]
+        L.jo_page_demand.argtypes = [i32, P, P, i32, P, i32, P, i32, i32, P, i32, P, P, P]
         L.jo_runs.argtypes = [P, i32, i32, P, P]
         L.jo_predict_diff.argtypes = [P, P, i32, i32, P, P, P]
-        L.jo_sparse_attn.argtypes = [i32, P, P, i32, P, P, i32, i32, i32, P, P, i64, i64,
+        L.jo_sparse_attn.argtypes = [i32, P, P, i32, i32, P, P, i32, i32, i32, P, P, i64, i64,
                                      P, i32, i32, P, i32, dbl, P, P]
         for f in ("jo_index_scores", "jo_topk", "jo_topk_sharded", "jo_page_demand", "jo_runs",
                   "jo_predict_diff", "jo_sparse_attn"):
@@ -92,7 +92,7 @@ def e8m0_value(e: int) -> float:
     return lib().jo_e8m0_value(int(e))
 
 
-def index_scores_mxfp4(q_start, hist_len, q, q_dt, q_scale, kI, k_bscale, k_scale, w, rows, out_ld=None):
+def index_scores_mxfp4(q_start, hist_len, q, q_dt, q_scale, kI, k_bscale, k_scale, w, rows, out_ld=None, entry=1):
     """Scores (float64) with MXFP4 indexer keys: kI [ctx rows, d/2] bytes,
     k_bscale [ctx rows, d/32] E8M0 bytes."""
     q_start = _c(q_start, np.int32)
@@ -100,9 +100,10 @@ def index_scores_mxfp4(q_start, hist_len, q, q_dt, q_scale, kI, k_bscale, k_scal
     rows = _c(rows, np.int32)
     H, d = q.shape[1], q.shape[2]
     if out_ld is None:
-        out_ld = int((hist_len + np.diff(q_start)).max())
+        out_ld = int(((hist_len + np.diff(q_start)) // entry).max())
     out = np.empty((rows.shape[0], out_ld), dtype=np.float64)
-    rc = lib().jo_index_scores_mxfp4(len(hist_len), _p(q_start), _p(hist_len), _p(np.ascontiguousarray(q)), DT[q_dt],
+    rc = lib().jo_index_scores_mxfp4(len(hist_len), _p(q_start), _p(hist_len), entry, _p(np.ascontiguousarray(q)),
+                                     DT[q_dt],
                                      _p(_c(q_scale, np.float32)), _p(_c(kI, np.uint8)), _p(_c(k_bscale, np.uint8)),
                                      _p(_c(k_scale, np.float32)), _p(_c(w, np.float32)), H, d, rows.shape[0],
                                      _p(rows), _p(out), out_ld)
@@ -114,16 +115,17 @@ def bf16_value(b: int) -> float:
     return lib().jo_bf16_value(int(b))
 
 
-def index_scores(q_start, hist_len, q, q_dt, q_scale, kI, k_dt, k_scale, w, rows, out_ld=None):
-    """Scores (float64) of the given global query rows, [len(rows), out_ld]."""
+def index_scores(q_start, hist_len, q, q_dt, q_scale, kI, k_dt, k_scale, w, rows, out_ld=None, entry=1):
+    """Scores (float64) of the given global query rows, [len(rows), out_ld].
+    entry = tokens per entry (1: token granularity)."""
     q_start = _c(q_start, np.int32)
     hist_len = _c(hist_len, np.int32)
     rows = _c(rows, np.int32)
     H, d = q.shape[1], q.shape[2]
     if out_ld is None:
-        out_ld = int((hist_len + np.diff(q_start)).max())
+        out_ld = int(((hist_len + np.diff(q_start)) // entry).max())
     out = np.empty((rows.shape[0], out_ld), dtype=np.float64)
-    rc = lib().jo_index_scores(len(hist_len), _p(q_start), _p(hist_len), _p(np.ascontiguousarray(q)), DT[q_dt],
+    rc = lib().jo_index_scores(len(hist_len), _p(q_start), _p(hist_len), entry, _p(np.ascontiguousarray(q)), DT[q_dt],
                                _p(_c(q_scale, np.float32)), _p(np.ascontiguousarray(kI)), DT[k_dt],
                                _p(_c(k_scale, np.float32)), _p(_c(w, np.float32)), H, d,
                                rows.shape[0], _p(rows), _p(out), out_ld)
@@ -131,20 +133,20 @@ def index_scores(q_start, hist_len, q, q_dt, q_scale, kI, k_dt, k_scale, w, rows
     return out
 
 
-def topk(q_start, hist_len, rows, scores_rows, k):
+def topk(q_start, hist_len, rows, scores_rows, k, entry=1):
     """Top-k ids of the given rows; scores_rows [len(rows), ld] float32."""
     q_start = _c(q_start, np.int32)
     hist_len = _c(hist_len, np.int32)
     rows = _c(rows, np.int32)
     sc = _c(scores_rows, np.float32)
     out = np.empty((rows.shape[0], k), dtype=np.int32)
-    rc = lib().jo_topk(len(hist_len), _p(q_start), _p(hist_len), rows.shape[0], _p(rows), _p(sc),
+    rc = lib().jo_topk(len(hist_len), _p(q_start), _p(hist_len), entry, rows.shape[0], _p(rows), _p(sc),
                        sc.shape[1], k, _p(out))
     _check(rc, "topk")
     return out
 
 
-def topk_sharded(q_start, hist_len, rows, scores_rows, k, shards, align):
+def topk_sharded(q_start, hist_len, rows, scores_rows, k, shards, align, entry=1):
     """Per-shard top-(k/shards) history ids of the given rows (Eq. 3);
     scores_rows [len(rows), ld] float32.  Returns [len(rows), k]."""
     q_start = _c(q_start, np.int32)
@@ -152,13 +154,13 @@ def topk_sharded(q_start, hist_len, rows, scores_rows, k, shards, align):
     rows = _c(rows, np.int32)
     sc = _c(scores_rows, np.float32)
     out = np.empty((rows.shape[0], k), dtype=np.int32)
-    rc = lib().jo_topk_sharded(len(hist_len), _p(q_start), _p(hist_len), rows.shape[0], _p(rows), _p(sc),
+    rc = lib().jo_topk_sharded(len(hist_len), _p(q_start), _p(hist_len), entry, rows.shape[0], _p(rows), _p(sc),
                                sc.shape[1], k, shards, align, _p(out))
     _check(rc, "topk_sharded")
     return out
 
 
-def page_demand(q_start, hist_len, topk_idx, page_table, page_size, num_phys_pages, limit=None):
+def page_demand(q_start, hist_len, topk_idx, page_table, page_size, num_phys_pages, limit=None, entry=1):
     """(bitmap uint32 [ceil(P/32)], ascending page list, count)."""
     q_start = _c(q_start, np.int32)
     hist_len = _c(hist_len, np.int32)
@@ -169,7 +171,7 @@ def page_demand(q_start, hist_len, topk_idx, page_table, page_size, num_phys_pag
     bm = np.zeros(max(nw, 1), dtype=np.uint32)
     lst = np.zeros(max(num_phys_pages, 1), dtype=np.int32)
     cnt = np.zeros(1, dtype=np.int32)
-    rc = lib().jo_page_demand(len(hist_len), _p(q_start), _p(hist_len), _p(ti), ti.shape[1], _p(pt),
+    rc = lib().jo_page_demand(len(hist_len), _p(q_start), _p(hist_len), entry, _p(ti), ti.shape[1], _p(pt),
                               pt.shape[1], page_size, _p(lim), num_phys_pages, _p(bm), _p(lst), _p(cnt))
     _check(rc, "page_demand")
     c = int(cnt[0])
@@ -200,7 +202,7 @@ def predict_diff(actual, predicted, num_phys_pages, max_run):
 
 
 def sparse_attn(q_start, hist_len, rows, q_rows, k_pool, v_pool, k_row_stride, v_row_stride,
-                page_table, page_size, sel_rows, scale, dv):
+                page_table, page_size, sel_rows, scale, dv, entry=1):
     """Attention (float64) for the given rows.
 
     q_rows [len(rows), Hq, dqk] bf16 bits of those rows; sel_rows [len(rows), k].
@@ -217,7 +219,7 @@ def sparse_attn(q_start, hist_len, rows, q_rows, k_pool, v_pool, k_row_stride, v
     vp = kp if v_pool is None else _c(v_pool, np.uint16)
     pt = _c(page_table, np.int32)
     sel = _c(sel_rows, np.int32)
-    rc = lib().jo_sparse_attn(len(hist_len), _p(q_start), _p(hist_len), n, _p(rows), _p(q_rows), Hq, dqk, dv,
+    rc = lib().jo_sparse_attn(len(hist_len), _p(q_start), _p(hist_len), entry, n, _p(rows), _p(q_rows), Hq, dqk, dv,
                               _p(kp), _p(vp), k_row_stride, v_row_stride, _p(pt), pt.shape[1], page_size,
                               _p(sel), sel.shape[1], float(scale), _p(out), _p(lse))
     _check(rc, "sparse_attn")

@@ -34,6 +34,12 @@
  *     pieces of at most max_run pages.
  *   - sparse attention over the selected tokens only: the paragraph after
  *     Eq. (1) (KV of the selected tokens feed core attention).
+ *   - entry granularity (Sec. "Sparse Attention", footnote on DeepSeek-V4;
+ *     the notation table applies unchanged): a candidate is an entry, one
+ *     cached row standing for E consecutive tokens, E*j .. E*j + E - 1, which
+ *     a token can select once the entry's last token precedes or is itself.
+ *     Every function takes E (tokens per entry; 1 = token granularity) and
+ *     counts ids, key rows and score columns in entries.
  *
  * Every function returns 0 on success and a negative value on bad arguments.
  */
@@ -90,21 +96,36 @@ static int session_of(int nseq, const int32_t *q_start, int row)
     return b;
 }
 
-static int64_t key_base(const int32_t *q_start, const int32_t *hist_len, int b)
+/* Entry j (tokens E*j .. E*j+E-1) is a candidate at position p when its
+ * last token is at or before p. */
+static int entry_complete(int64_t j, int E, int64_t p)
+{
+    return (int64_t)E * j + (E - 1) <= p;
+}
+
+/* Entries whose whole region lies within the first n tokens. */
+static int64_t whole_entries(int64_t n, int E)
+{
+    return n / E;
+}
+
+/* First key row of session b: the entries of the sessions before it. */
+static int64_t key_base(const int32_t *q_start, const int32_t *hist_len, int b, int E)
 {
     int64_t base = 0;
     for (int j = 0; j < b; j++)
-        base += (int64_t)hist_len[j] + (q_start[j + 1] - q_start[j]);
+        base += whole_entries((int64_t)hist_len[j] + (q_start[j + 1] - q_start[j]), E);
     return base;
 }
 
 /*
  * Indexer scores for a subset of query rows.
  * q [total_q, H, d] (dtype q_dt), q_scale [total_q] or NULL (= 1);
- * kI [total_ctx, d] (dtype k_dt), rows of session b start at the sum of the
- * earlier sessions' M_b + N_b; k_scale [total_ctx] or NULL; w [total_q, H].
- * out[r * out_ld + s] for s < out_ld: the score of candidate s, -inf beyond
- * the causal limit M_b + i (and beyond the session's context).
+ * kI [total_ctx, d] (dtype k_dt), one row per token or entry; rows of session
+ * b start after the earlier sessions' rows; k_scale [total_ctx] or NULL;
+ * w [total_q, H].  out[r * out_ld + s] for s < out_ld: the score of candidate
+ * s, -inf for ids the token cannot select yet (tokens: beyond M_b + i) and
+ * beyond the session's rows.
  */
 /*
  * OCP MX FP4 (e2m1): sign, two exponent bits (bias 1), one mantissa bit; an
@@ -136,24 +157,24 @@ static double mxfp4_elem(const uint8_t *k, const uint8_t *bscale, int64_t row, i
     return jo_e2m1_value(code) * jo_e8m0_value(bscale[row * (d / 32) + j / 32]);
 }
 
-static int index_scores_impl(int nseq, const int32_t *q_start, const int32_t *hist_len,
+static int index_scores_impl(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
                              const void *q, int q_dt, const float *q_scale,
                              const void *kI, int k_dt, const uint8_t *k_bscale, const float *k_scale,
                              const float *w, int H, int d,
                              int nrows, const int32_t *rows, double *out, int64_t out_ld);
 
-int jo_index_scores(int nseq, const int32_t *q_start, const int32_t *hist_len,
+int jo_index_scores(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
                     const void *q, int q_dt, const float *q_scale,
                     const void *kI, int k_dt, const float *k_scale,
                     const float *w, int H, int d,
                     int nrows, const int32_t *rows, double *out, int64_t out_ld)
 {
-    return index_scores_impl(nseq, q_start, hist_len, q, q_dt, q_scale, kI, k_dt, NULL, k_scale, w, H, d, nrows,
-                             rows, out, out_ld);
+    return index_scores_impl(nseq, q_start, hist_len, E, q, q_dt, q_scale, kI, k_dt, NULL, k_scale, w, H, d,
+                             nrows, rows, out, out_ld);
 }
 
 /* Eq. 1's scores with MXFP4 indexer keys (kI: [ctx rows][d/2] bytes, k_bscale: [ctx rows][d/32] E8M0). */
-int jo_index_scores_mxfp4(int nseq, const int32_t *q_start, const int32_t *hist_len,
+int jo_index_scores_mxfp4(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
                           const void *q, int q_dt, const float *q_scale,
                           const uint8_t *kI, const uint8_t *k_bscale, const float *k_scale,
                           const float *w, int H, int d,
@@ -161,17 +182,17 @@ int jo_index_scores_mxfp4(int nseq, const int32_t *q_start, const int32_t *hist_
 {
     if (!k_bscale || d % 32 != 0)
         return -1;
-    return index_scores_impl(nseq, q_start, hist_len, q, q_dt, q_scale, kI, -1, k_bscale, k_scale, w, H, d, nrows,
-                             rows, out, out_ld);
+    return index_scores_impl(nseq, q_start, hist_len, E, q, q_dt, q_scale, kI, -1, k_bscale, k_scale, w, H, d,
+                             nrows, rows, out, out_ld);
 }
 
-static int index_scores_impl(int nseq, const int32_t *q_start, const int32_t *hist_len,
+static int index_scores_impl(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
                              const void *q, int q_dt, const float *q_scale,
                              const void *kI, int k_dt, const uint8_t *k_bscale, const float *k_scale,
                              const float *w, int H, int d,
                              int nrows, const int32_t *rows, double *out, int64_t out_ld)
 {
-    if (nseq < 1 || H < 1 || d < 1 || nrows < 0)
+    if (nseq < 1 || H < 1 || d < 1 || nrows < 0 || E < 1)
         return -1;
     int bad = 0;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -184,15 +205,15 @@ static int index_scores_impl(int nseq, const int32_t *q_start, const int32_t *hi
         int b = session_of(nseq, q_start, g);
         int i = g - q_start[b];
         int64_t M = hist_len[b];
-        int64_t ctx = M + (q_start[b + 1] - q_start[b]);
-        int64_t kb = key_base(q_start, hist_len, b);
+        int64_t ctx = whole_entries(M + (q_start[b + 1] - q_start[b]), E);
+        int64_t kb = key_base(q_start, hist_len, b, E);
         double sq = q_scale ? (double)q_scale[g] : 1.0;
         double *qd = (double *)malloc(sizeof(double) * (size_t)H * d);
         for (int64_t e = 0; e < (int64_t)H * d; e++)
             qd[e] = elem(q, q_dt, (int64_t)g * H * d + e);
         double *kd = (double *)malloc(sizeof(double) * (size_t)d);
         for (int64_t s = 0; s < out_ld; s++) {
-            if (s > M + i || s >= ctx) {
+            if (!entry_complete(s, E, M + i) || s >= ctx) {
                 out[(int64_t)r * out_ld + s] = -INFINITY;
                 continue;
             }
@@ -232,14 +253,15 @@ static int cand_cmp(const void *a, const void *b)
 
 /*
  * Top-k per query row (Eq. 1 selection).  scores[r * ld + s] holds row r's
- * fp32 scores (r indexes the given rows); candidates are s in [0, M_b + i].
+ * fp32 scores (r indexes the given rows); candidates are the ids s the token
+ * at position M_b + i can select (tokens: s in [0, M_b + i]).
  * out[r * k + j]: the selected ids in (score desc, id asc) order, then -1.
  */
-int jo_topk(int nseq, const int32_t *q_start, const int32_t *hist_len,
+int jo_topk(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
             int nrows, const int32_t *rows, const float *scores, int64_t ld,
             int k, int32_t *out)
 {
-    if (nseq < 1 || k < 1 || nrows < 0)
+    if (nseq < 1 || k < 1 || nrows < 0 || E < 1)
         return -1;
     int bad = 0;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -250,9 +272,10 @@ int jo_topk(int nseq, const int32_t *q_start, const int32_t *hist_len,
             continue;
         }
         int b = session_of(nseq, q_start, g);
-        int64_t n = (int64_t)hist_len[b] + (g - q_start[b]) + 1;
-        if (n > ld)
-            n = ld;
+        int64_t pos = (int64_t)hist_len[b] + (g - q_start[b]);
+        int64_t n = 0; /* candidates form a prefix of the ids */
+        while (n < ld && entry_complete(n, E, pos))
+            n++;
         jo_cand *c = (jo_cand *)malloc(sizeof(jo_cand) * (size_t)(n > 0 ? n : 1));
         for (int64_t s = 0; s < n; s++) {
             double v = (double)scores[(int64_t)r * ld + s];
@@ -278,11 +301,11 @@ int jo_topk(int nseq, const int32_t *q_start, const int32_t *hist_len,
  * out[r * k + n * (k/G) + j]: shard n's selected ids in (score desc, id asc)
  * order, then -1.  Requires k % G == 0.
  */
-int jo_topk_sharded(int nseq, const int32_t *q_start, const int32_t *hist_len,
+int jo_topk_sharded(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
                     int nrows, const int32_t *rows, const float *scores, int64_t ld,
                     int k, int G, int align, int32_t *out)
 {
-    if (nseq < 1 || k < 1 || G < 1 || k % G != 0 || align < 1 || nrows < 0)
+    if (nseq < 1 || k < 1 || G < 1 || k % G != 0 || align < 1 || nrows < 0 || E < 1)
         return -1;
     const int kg = k / G;
     int bad = 0;
@@ -294,9 +317,9 @@ int jo_topk_sharded(int nseq, const int32_t *q_start, const int32_t *hist_len,
             continue;
         }
         int b = session_of(nseq, q_start, g);
-        int64_t M = hist_len[b];
-        if (M > ld)
-            M = ld;
+        int64_t M = 0; /* history ids: entries complete before the append */
+        while (M < ld && entry_complete(M, E, (int64_t)hist_len[b] - 1))
+            M++;
         int64_t units = (M + align - 1) / align;
         int64_t L = (int64_t)align * ((units + G - 1) / G);
         jo_cand *c = (jo_cand *)malloc(sizeof(jo_cand) * (size_t)(L > 0 ? L : 1));
@@ -321,25 +344,27 @@ int jo_topk_sharded(int nseq, const int32_t *q_start, const int32_t *hist_len,
 
 /*
  * Page-demand set: A = { pt_b[s / page_size] : s selected by any row of
- * session b, 0 <= s < min(limit_b, M_b + N_b) }, over a shared physical pool.
+ * session b, 0 <= s < min(limit_b, C_b) }, over a shared physical pool, with
+ * C_b the session's ids (tokens: M_b + N_b).
  * topk_idx [total_q, k] session-local ids (others are padding);
- * page_table [nseq, pt_ld]; limit [nseq] or NULL (= M_b, history only).
+ * page_table [nseq, pt_ld]; limit [nseq] or NULL (= the history ids, the
+ * entries wholly within the first M_b tokens).
  * bitmap [ceil(P/32)] (bit p%32 of word p/32); list ascending; *count.
  */
-int jo_page_demand(int nseq, const int32_t *q_start, const int32_t *hist_len,
+int jo_page_demand(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
                    const int32_t *topk_idx, int k,
                    const int32_t *page_table, int pt_ld, int page_size,
                    const int32_t *limit, int num_phys_pages,
                    uint32_t *bitmap, int32_t *page_list, int32_t *count)
 {
-    if (nseq < 1 || k < 1 || page_size < 1 || num_phys_pages < 0)
+    if (nseq < 1 || k < 1 || page_size < 1 || num_phys_pages < 0 || E < 1)
         return -1;
     int nwords = (num_phys_pages + 31) / 32;
     unsigned char *sel = (unsigned char *)calloc((size_t)num_phys_pages + 1, 1);
     int bad = 0;
     for (int b = 0; b < nseq; b++) {
-        int64_t ctx = (int64_t)hist_len[b] + (q_start[b + 1] - q_start[b]);
-        int64_t lim = limit ? limit[b] : hist_len[b];
+        int64_t ctx = whole_entries((int64_t)hist_len[b] + (q_start[b + 1] - q_start[b]), E);
+        int64_t lim = limit ? limit[b] : whole_entries(hist_len[b], E);
         if (lim > ctx)
             lim = ctx;
         for (int g = q_start[b]; g < q_start[b + 1]; g++) {
@@ -452,12 +477,13 @@ int jo_predict_diff(const uint32_t *actual, const uint32_t *predicted, int num_p
  *   k_pool + ((pt_b[s / page_size] * page_size) + s % page_size) * k_row_stride,
  * its first dqk elements; V row likewise from v_pool, first dv elements (for
  * the latent-KV layout v_pool == k_pool and V is the head of the K row).
- * sel [nrows, k]: row r's selected ids; ids outside [0, M_b + i] are padding.
+ * sel [nrows, k]: row r's selected ids; ids the token cannot select (tokens:
+ * outside [0, M_b + i]) are padding.
  * out [nrows, Hq, dv]: softmax_s(scale * q.K_s) weighted sum of V_s;
  * lse [nrows, Hq] (may be NULL): log-sum-exp of the scaled logits.
  * A row with no valid id gives out = 0 and lse = -inf.
  */
-int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len,
+int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
                    int nrows, const int32_t *rows,
                    const uint16_t *q, int Hq, int dqk, int dv,
                    const uint16_t *k_pool, const uint16_t *v_pool,
@@ -466,7 +492,7 @@ int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len,
                    const int32_t *sel, int k, double scale,
                    double *out, double *lse)
 {
-    if (nseq < 1 || Hq < 1 || dqk < 1 || dv < 1 || k < 1 || page_size < 1 || nrows < 0)
+    if (nseq < 1 || Hq < 1 || dqk < 1 || dv < 1 || k < 1 || page_size < 1 || nrows < 0 || E < 1)
         return -1;
     int bad = 0;
 #pragma omp parallel for schedule(dynamic, 1)
@@ -477,14 +503,14 @@ int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len,
             continue;
         }
         int b = session_of(nseq, q_start, g);
-        int64_t lim = (int64_t)hist_len[b] + (g - q_start[b]); /* last causal id */
+        int64_t pos = (int64_t)hist_len[b] + (g - q_start[b]); /* the token's position */
         double *logit = (double *)malloc(sizeof(double) * (size_t)k);
         int64_t *krow = (int64_t *)malloc(sizeof(int64_t) * (size_t)k);
         int64_t *vrow = (int64_t *)malloc(sizeof(int64_t) * (size_t)k);
         int nv = 0;
         for (int j = 0; j < k; j++) {
             int64_t s = sel[(int64_t)r * k + j];
-            if (s < 0 || s > lim)
+            if (s < 0 || !entry_complete(s, E, pos))
                 continue;
             int64_t lp = s / page_size;
             if (lp >= pt_ld) {

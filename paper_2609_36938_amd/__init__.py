@@ -37,6 +37,7 @@ class _Batch(ctypes.Structure):
         ("ctx_start", ctypes.c_void_p),
         ("hist_len", ctypes.c_void_p),
         ("score_start", ctypes.c_void_p),
+        ("entry_shift", ctypes.c_int32),
     ]
 
 
@@ -104,14 +105,17 @@ def _dtype_code(t: torch.Tensor, dt: Optional[str]) -> int:
 
 
 class Batch:
-    """A ragged batch of sessions: history lengths M_b and appended lengths N_b."""
+    """A ragged batch of sessions: history lengths M_b and appended lengths N_b
+    (tokens).  entry_shift = e > 0 selects entry granularity: candidates are
+    entries of 2^e tokens, and session b holds (M_b + N_b) >> e of them."""
 
-    def __init__(self, hist_len: Sequence[int], new_len: Sequence[int], device="cuda"):
+    def __init__(self, hist_len: Sequence[int], new_len: Sequence[int], device="cuda", entry_shift: int = 0):
         hl = np.asarray(hist_len, dtype=np.int64).reshape(-1)
         nl = np.asarray(new_len, dtype=np.int64).reshape(-1)
         if hl.shape != nl.shape or hl.size < 1:
             raise JanusError("hist_len and new_len must be equal-length, non-empty")
-        ctx = hl + nl
+        self.entry_shift = int(entry_shift)
+        ctx = (hl + nl) >> self.entry_shift
         self.hist_len_host = hl.astype(np.int32)
         self.new_len_host = nl.astype(np.int32)
         self.q_start_host = np.concatenate([[0], np.cumsum(nl)]).astype(np.int32)
@@ -127,7 +131,7 @@ class Batch:
         self.total_scores = int(self.score_start_host[-1])
         self.c = _Batch(len(hl), self.total_q, int(nl.max()), self.max_ctx, self.total_ctx,
                         self.q_start.data_ptr(), self.ctx_start.data_ptr(), self.hist_len.data_ptr(),
-                        self.score_start.data_ptr())
+                        self.score_start.data_ptr(), self.entry_shift)
 
     @property
     def ref(self):

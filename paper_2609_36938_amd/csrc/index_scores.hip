@@ -259,7 +259,7 @@ JANUS_DEV bool xcd_tile_chunk(int L, int nchunks, int ntiles, int &tile, int &ch
 template <int H, int TPW>
 __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
-    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs,
+    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs, int es,
     int nchunks, int key_chunk, int ntiles, const uint8_t *__restrict__ q, const float *__restrict__ q_scale,
     const uint8_t *__restrict__ kI, const float *__restrict__ k_scale, const float *__restrict__ w,
     float *__restrict__ scores)
@@ -281,7 +281,7 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
         return;
     const int N = q_start[b + 1] - q_start[b];
     const int M = hist_len[b];
-    const int ctx = M + N;
+    const int ctx = entries_of(M + N, es);
     const int key_lo = chunk * key_chunk;
     if (key_lo >= ctx)
         return;
@@ -294,7 +294,7 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     const int qrow0 = q_start[b];
     const int64_t kbase = ctx_start[b];
     // block-wide causal limit: stages past it need no keys
-    const int block_lim = M + min(tile0 + TOK_TILE - 1, N - 1);
+    const int block_lim = last_cand(M, min(tile0 + TOK_TILE - 1, N - 1), es);
     const int key_end = min(key_hi, block_lim + 1);
 
     // Key DMA: lane L of wave instruction i (i = wave + 4j, j < 4) fills
@@ -350,8 +350,8 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
         wv[hb][0] = __builtin_convertvector((v2f){t[0] * sq, t[1] * sq}, v2bf);
         wv[hb][1] = __builtin_convertvector((v2f){t[2] * sq, t[3] * sq}, v2bf);
     }
-    const int lim = M + e_tok;  // last causal candidate of this lane's token
-    const int wave_lim = M + min(tw0 + TPW - 1, N - 1);
+    const int lim = last_cand(M, e_tok, es);  // last causal candidate of this lane's token
+    const int wave_lim = last_cand(M, min(tw0 + TPW - 1, N - 1), es);
     int scales = IDX_MFMA_SCALES;
     // this lane's two 16-byte columns (2*kg, 2*kg+1) of LDS row 16*j + r16
     const int g8 = (r16 >> 1) & 7;
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     constexpr int STORES_PER_GROUP = 4 / GPT;
     constexpr int STAGE_STORES = (IDX_STAGE / 64) * STORES_PER_GROUP;
     // every token of the block sees all keys below this bound
-    const int interior_end = min(ctx, M + tile0 + 1);
+    const int interior_end = min(ctx, last_cand(M, tile0, es) + 1);
 
     // one stage: compute the keys in (stg, ks) while the next stage streams in
     auto stage = [&](int k0, const uint8_t *stg, const float *ks) {
@@ -453,7 +453,7 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
 // Plain vector kernel for any dtype and shape: one (token, key) score per thread.
 __global__ __launch_bounds__(256) void index_scores_vector(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
-    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs,
+    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs, int es,
     const void *__restrict__ q, int q_dt, const float *__restrict__ q_scale,
     const void *__restrict__ kI, int k_dt, const float *__restrict__ k_scale,
     const float *__restrict__ w, int H, int d, float *__restrict__ scores)
@@ -463,13 +463,13 @@ __global__ __launch_bounds__(256) void index_scores_vector(
         return;
     const int N = q_start[b + 1] - q_start[b];
     const int M = hist_len[b];
-    const int ctx = M + N;
+    const int ctx = entries_of(M + N, es);
     const int i = t0 + threadIdx.x / GEN_KEY_TILE;
     const int s = blockIdx.x * GEN_KEY_TILE + threadIdx.x % GEN_KEY_TILE;
     if (i >= N || s >= ctx)
         return;
     float *dst = scores + score_start[b] + (int64_t)i * ctx + s;
-    if (s > M + i) {
+    if (s > last_cand(M, i, es)) {
         *dst = -INFINITY;
         return;
     }
@@ -507,7 +507,7 @@ constexpr int ROWS_CHUNK = 4096;   // keys per block
 template <int NQ, bool FP4>
 __global__ __launch_bounds__(256, 2) void index_scores_rows(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
-    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs, int nchunks,
+    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs, int es, int nchunks,
     int one_tile, const uint8_t *__restrict__ q, const float *__restrict__ q_scale, const uint8_t *__restrict__ kI,
     const uint8_t *__restrict__ k_bscale, const float *__restrict__ k_scale, const float *__restrict__ w,
     float *__restrict__ scores)
@@ -520,7 +520,7 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
     if (!one_tile && !tile_slot(q_start, num_seqs, tile, NQ, b, t0))
         return;
     const int qs = q_start[b], N = q_start[b + 1] - qs;
-    const int M = hist_len[b], ctx = M + N;
+    const int M = hist_len[b], ctx = entries_of(M + N, es);
     const int nv = min(NQ, N - t0);  // tokens of this tile
     if (nv <= 0 || c0 >= ctx)
         return;
@@ -572,7 +572,11 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
     const __amdgpu_buffer_rsrc_t srs =
         make_buffer_rsrc(scores + score_start[b] + (int64_t)t0 * ctx, (uint32_t)(nv * ctx) << 2);
     const int ngroups = (min(ROWS_CHUNK, ctx - c0) + 63) / 64;
-    const int last_lim = M + t0 + nv - 1;  // largest causal limit in the tile
+    int lim[NQ];  // each token's last candidate (block-uniform)
+#pragma unroll
+    for (int t = 0; t < NQ; ++t)
+        lim[t] = __builtin_amdgcn_readfirstlane(last_cand(M, t0 + t, es));
+    const int last_lim = last_cand(M, t0 + nv - 1, es);  // largest causal limit in the tile
 
     struct Group {
         v4i k[8];   // 16-key block j: key row 16j + r16; fp8: bytes 32kg.. in k[2j], k[2j+1]; fp4: both halves in k[j]
@@ -632,7 +636,7 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
             if (t >= nv)
                 continue;
             float v = kg == 0 ? res[t][0] : kg == 1 ? res[t][1] : kg == 2 ? res[t][2] : res[t][3];
-            v = s > M + t0 + t ? -INFINITY : v * G.ks;
+            v = s > lim[t] ? -INFINITY : v * G.ks;
             const uint32_t off = s < ctx ? (uint32_t)(t * ctx + s) * 4u : 0x80000000u;
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), srs, off, 0, 0);
         }
@@ -679,7 +683,7 @@ static void launch_rows(const janus_batch *bt, const void *q, const float *q_sca
     const dim3 grid((unsigned)(rows_tiles(bt, nq) * nchunks));
     auto go = [&](auto kern) {
         hipLaunchKernelGGL(kern, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start, bt->hist_len, bt->score_start,
-                           bt->num_seqs, nchunks, one_tile, (const uint8_t *)q, q_scale, (const uint8_t *)kI,
+                           bt->num_seqs, bt->entry_shift, nchunks, one_tile, (const uint8_t *)q, q_scale, (const uint8_t *)kI,
                            k_bscale, k_scale, w, scores);
     };
     if (nq == 1)
@@ -728,13 +732,13 @@ extern "C" int janus_index_scores(const janus_batch *bt, const void *q, janus_dt
         const int ntiles = ceil_div(bt->total_q, 4 * TPW) + nseq;
         const int per_xcd = ceil_div(nchunks, IDX_XCD) * ntiles;
         hipLaunchKernelGGL((index_scores_fp8_mfma<64, TPW>), dim3(IDX_XCD * per_xcd), dim3(256), 0, st, bt->q_start,
-                           bt->ctx_start, bt->hist_len, bt->score_start, nseq, nchunks, key_chunk, ntiles,
+                           bt->ctx_start, bt->hist_len, bt->score_start, nseq, bt->entry_shift, nchunks, key_chunk, ntiles,
                            (const uint8_t *)q, q_scale, (const uint8_t *)kI, k_scale, w, scores);
         return launch_status();
     }
     dim3 grid(ceil_div(bt->max_ctx, GEN_KEY_TILE), ceil_div(bt->total_q, GEN_TOK_TILE) + nseq);
     hipLaunchKernelGGL(index_scores_vector, grid, dim3(GEN_TOK_TILE * GEN_KEY_TILE), 0, st, bt->q_start,
-                       bt->ctx_start, bt->hist_len, bt->score_start, nseq, q, (int)q_dt, q_scale, kI, (int)k_dt,
+                       bt->ctx_start, bt->hist_len, bt->score_start, nseq, bt->entry_shift, q, (int)q_dt, q_scale, kI, (int)k_dt,
                        k_scale, w, H, d, scores);
     return launch_status();
 }

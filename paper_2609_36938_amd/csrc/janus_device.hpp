@@ -21,6 +21,12 @@ typedef short v2s __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
+// Entry granularity (2^es tokens per entry; es = 0: tokens).  Entries
+// complete among a session's first n tokens, and the last candidate of the
+// appended token at position M + i: the last entry complete there.
+JANUS_DEV int entries_of(int n, int es) { return n >> es; }
+JANUS_DEV int last_cand(int M, int i, int es) { return ((M + i + 1) >> es) - 1; }
+
 // Session of global query row `row`: largest b with q_start[b] <= row.
 JANUS_DEV int session_of_row(const int32_t *q_start, int num_seqs, int row)
 {

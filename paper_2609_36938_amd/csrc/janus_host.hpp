@@ -22,7 +22,7 @@ inline bool batch_ok(const janus_batch *b)
 {
     return b && b->num_seqs >= 1 && b->total_q >= 0 && b->max_q >= 0 && b->max_ctx >= 0 &&
            b->total_ctx >= 0 && b->q_start && b->hist_len && b->max_q <= b->total_q &&
-           (int64_t)b->max_ctx <= b->total_ctx;
+           (int64_t)b->max_ctx <= b->total_ctx && b->entry_shift >= 0 && b->entry_shift <= 16;
 }
 
 inline bool dtype_ok(int dt) { return dt == JANUS_F32 || dt == JANUS_BF16 || dt == JANUS_FP8_E4M3; }

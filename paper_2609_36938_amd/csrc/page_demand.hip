@@ -30,7 +30,7 @@ __global__ void bitmap_zero(uint32_t *__restrict__ bm, int nwords)
 }
 
 __global__ __launch_bounds__(PD_THREADS) void page_union(
-    const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs, int total_q,
+    const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs, int es, int total_q,
     const int32_t *__restrict__ topk_idx, int k, const int32_t *__restrict__ page_table, int pt_ld,
     int page_shift, const int32_t *__restrict__ limit, int nwords, uint32_t *__restrict__ bitmap)
 {
@@ -45,8 +45,8 @@ __global__ __launch_bounds__(PD_THREADS) void page_union(
     for (int r = r0; r < r1; ++r) {
         while (r >= q_start[b + 1])
             ++b;
-        const int ctx = hist_len[b] + (q_start[b + 1] - q_start[b]);
-        const int lim = min(ctx, limit ? limit[b] : hist_len[b]);
+        const int ctx = entries_of(hist_len[b] + (q_start[b + 1] - q_start[b]), es);
+        const int lim = min(ctx, limit ? limit[b] : entries_of(hist_len[b], es));
         const int32_t *row = topk_idx + (int64_t)r * k;
         const int32_t *pt = page_table + (int64_t)b * pt_ld;
         for (int j = threadIdx.x; j < k; j += PD_THREADS) {
@@ -290,7 +290,8 @@ extern "C" int janus_page_demand(const janus_batch *bt, const int32_t *topk_idx,
                                                 std::max<int64_t>(1, entries / (PD_THREADS * 16)));
         const int shift = __builtin_ctz((unsigned)page_size);
         hipLaunchKernelGGL(page_union, dim3(nblk), dim3(PD_THREADS), nwords * sizeof(uint32_t), st, bt->q_start,
-                           bt->hist_len, bt->num_seqs, bt->total_q, topk_idx, k, page_table, pt_ld, shift, limit,
+                           bt->hist_len, bt->num_seqs, bt->entry_shift, bt->total_q, topk_idx, k, page_table, pt_ld,
+                           shift, limit,
                            nwords, bitmap);
     }
     hipLaunchKernelGGL(page_list_runs, dim3(1), dim3(RUN_THREADS), 0, st, bitmap, num_phys_pages, max_run,

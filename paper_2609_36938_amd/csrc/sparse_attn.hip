@@ -83,7 +83,7 @@ constexpr int mla_buf_bytes() { return NW * mla_ipw<NW>() * 64 * 16; }
 
 template <int NW, bool SPLIT>
 __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
-    const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs,
+    const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs, int es,
     const uint16_t *__restrict__ q, const uint16_t *__restrict__ kv, int64_t row_stride,
     const int32_t *__restrict__ page_table, int pt_ld, int page_shift, const int32_t *__restrict__ topk,
     int k, float scale_log2, void *__restrict__ out, int out_f32, float *__restrict__ lse, int num_splits,
@@ -117,7 +117,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         sel += j0;
     }
     const int b = session_of_row(q_start, num_seqs, g);
-    const int lim = hist_len[b] + (g - q_start[b]);  // last causal id
+    const int lim = last_cand(hist_len[b], g - q_start[b], es);  // last causal id
     const int32_t *pt = page_table + (int64_t)b * pt_ld;
     const int psz_mask = (1 << page_shift) - 1;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -442,7 +442,7 @@ constexpr int VEC_THREADS = 256;
 constexpr int VEC_MAX_DQK = 1024;
 
 __global__ __launch_bounds__(VEC_THREADS) void sparse_attn_vector(
-    const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs,
+    const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs, int es,
     const uint16_t *__restrict__ q, int Hq, int dqk, int dv, const uint16_t *__restrict__ k_pool,
     const uint16_t *__restrict__ v_pool, int64_t k_rs, int64_t v_rs, const int32_t *__restrict__ page_table,
     int pt_ld, int page_shift, const int32_t *__restrict__ topk, int k, float scale_log2,
@@ -454,7 +454,7 @@ __global__ __launch_bounds__(VEC_THREADS) void sparse_attn_vector(
     __shared__ float sred[VEC_THREADS / 64];
     const int g = blockIdx.x / Hq, h = blockIdx.x % Hq;
     const int b = session_of_row(q_start, num_seqs, g);
-    const int lim = hist_len[b] + (g - q_start[b]);
+    const int lim = last_cand(hist_len[b], g - q_start[b], es);
     const int32_t *pt = page_table + (int64_t)b * pt_ld;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     for (int e = tid; e < dqk; e += VEC_THREADS)
@@ -562,7 +562,7 @@ static void launch_mla(const janus_batch *bt, const void *q, int Hq, const void 
     const auto *kv = (const uint16_t *)k_pool;
     auto launch = [&](auto kern, int nw) {
         hipLaunchKernelGGL(kern, dim3(bt->total_q * splits), dim3(64 * nw), 0, st, bt->q_start, bt->hist_len,
-                           bt->num_seqs, qq, kv, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32,
+                           bt->num_seqs, bt->entry_shift, qq, kv, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32,
                            lse, splits, part);
     };
     if (part) {
@@ -621,7 +621,8 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
     if (dqk > VEC_MAX_DQK || dv > 4 * VEC_THREADS)
         return JANUS_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(sparse_attn_vector, dim3((int64_t)bt->total_q * Hq), dim3(VEC_THREADS), 0, st, bt->q_start,
-                       bt->hist_len, bt->num_seqs, (const uint16_t *)q, Hq, dqk, dv, (const uint16_t *)k_pool,
+                       bt->hist_len, bt->num_seqs, bt->entry_shift, (const uint16_t *)q, Hq, dqk, dv,
+                       (const uint16_t *)k_pool,
                        (const uint16_t *)v_pool, k_row_stride, v_row_stride, page_table, pt_ld, shift, topk_idx, k,
                        sl2, out, of32, lse);
     return launch_status();

@@ -441,26 +441,28 @@ JANUS_DEV void stream_row(TopkShared<CAP> &sm, const float *__restrict__ row, in
 template <int CAP>
 __global__ __launch_bounds__(TK_THREADS, CAP <= 4096 ? 4 : 2) void topk_rows(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len,
-    const int64_t *__restrict__ score_start, int num_seqs,
+    const int64_t *__restrict__ score_start, int num_seqs, int es,
     const float *__restrict__ scores, int k_row, int32_t *__restrict__ topk_idx, int shards, int align)
 {
     __shared__ TopkShared<CAP> sm;
-    // causal rows (shards == 0): block g selects k_row of [0, M+i];
+    // causal rows (shards == 0): block g selects k_row of its candidates
+    // (tokens: [0, M+i]);
     // sharded rows: block g*shards + n selects k_row/shards of history shard n
     const int g = shards ? blockIdx.x / shards : blockIdx.x;
     const int b = session_of_row(q_start, num_seqs, g);
     const int i = g - q_start[b];
     const int N = q_start[b + 1] - q_start[b];
     const int M = hist_len[b];
-    const int ctx = M + N;
-    int base = 0, n = M + i + 1, k = k_row;
+    const int ctx = entries_of(M + N, es);
+    const int Mh = entries_of(M, es);  // history candidates
+    int base = 0, n = last_cand(M, i, es) + 1, k = k_row;
     int32_t *out = topk_idx + (int64_t)g * k_row;
     if (shards) {
         const int sh = blockIdx.x - g * shards;
-        const int units = (M + align - 1) / align;        // pages of the history
-        const int L = align * ((units + shards - 1) / shards);  // tokens per shard
-        base = min(M, sh * L);
-        n = min(M, base + L) - base;
+        const int units = (Mh + align - 1) / align;        // pages of the history
+        const int L = align * ((units + shards - 1) / shards);  // candidates per shard
+        base = min(Mh, sh * L);
+        n = min(Mh, base + L) - base;
         k = k_row / shards;
         out += sh * k;
     }
@@ -578,10 +580,10 @@ static int launch_topk(const janus_batch *bt, const float *scores, int k, int32_
     const dim3 grid((unsigned)bt->total_q * (unsigned)(shards ? shards : 1));
     if (kk <= TK_SMALL_K && bt->max_ctx <= 2 * 4096 * 32)
         hipLaunchKernelGGL(topk_rows<4096>, grid, dim3(TK_THREADS), 0, as_stream(stream), bt->q_start, bt->hist_len,
-                           bt->score_start, bt->num_seqs, scores, k, topk_idx, shards, align);
+                           bt->score_start, bt->num_seqs, bt->entry_shift, scores, k, topk_idx, shards, align);
     else
         hipLaunchKernelGGL(topk_rows<8192>, grid, dim3(TK_THREADS), 0, as_stream(stream), bt->q_start, bt->hist_len,
-                           bt->score_start, bt->num_seqs, scores, k, topk_idx, shards, align);
+                           bt->score_start, bt->num_seqs, bt->entry_shift, scores, k, topk_idx, shards, align);
     return launch_status();
 }
 

@@ -146,3 +146,30 @@ def test_product_path_does_not_touch_the_oracle():
             if f.endswith((".py", ".hip", ".hpp", ".h", ".cpp")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert "import oracle" not in text and "janus_oracle" not in text, f
+
+
+def test_batch_layout_matches_the_header(tmp_path):
+    """The binding's janus_batch has the header's size and field offsets."""
+    import paper_2609_36938_amd as janus
+    src = tmp_path / "layout.c"
+    names = [f[0] for f in janus._Batch._fields_]
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "janus.h"\nint main(void){\n'
+                   + 'printf("%zu\\n", sizeof(janus_batch));\n'
+                   + "".join(f'printf("%zu\\n", offsetof(janus_batch, {n}));\n' for n in names) + "return 0;}\n")
+    exe = tmp_path / "layout"
+    subprocess.check_call(["gcc", "-std=c99", "-I", os.path.dirname(HEADER), "-o", str(exe), str(src)])
+    got = [int(x) for x in subprocess.check_output([str(exe)], text=True).split()]
+    assert got[0] == ctypes.sizeof(janus._Batch)
+    assert got[1:] == [getattr(janus._Batch, n).offset for n in names]
+
+
+def test_entry_shift_out_of_range_is_rejected(L):
+    ws = ctypes.c_size_t(0)
+    for shift in (-1, 17):
+        b = _batch()
+        b.entry_shift = shift
+        assert L.janus_topk(ctypes.byref(b), FAKE, 8, FAKE, None, ctypes.byref(ws), None) == 1
+        assert L.janus_index_scores(ctypes.byref(b), FAKE, 2, None, FAKE, 2, None, FAKE, 64, 128, FAKE, None) == 1
+    b = _batch()
+    b.entry_shift = 16
+    assert L.janus_topk(ctypes.byref(b), FAKE, 7000, FAKE, None, ctypes.byref(ws), None) == 2  # accepted shift

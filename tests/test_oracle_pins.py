@@ -536,3 +536,102 @@ def test_mxfp4_generator_rounding():
     assert codes == [0b0010, 0b0000, 0b0010, 0b0100, 0b0100, 0b0110, 0b0110, 0b0111, 0b1010]
     dec = _decode_mxfp4_table(packed, E)
     assert np.array_equal(dec[1, :4], x[1, :4])
+
+
+# ----------------------------------------------------------------------------- entry granularity
+# An entry j stands for tokens E*j .. E*j+E-1 (DeepSeek-V4 selects entries;
+# the notation table applies to them unchanged).  The pins below enumerate an
+# entry's tokens one by one, instead of the oracle's region-end comparison.
+
+def _entry_ok(j, E, pos):
+    """Every token of entry j is at or before position pos."""
+    return all(t <= pos for t in range(E * j, E * j + E))
+
+
+SMALL_MQA = dict(Hq=4, dqk=32, dv=32, mla=False, q_std=1.0, kv_std=1.0, scale=0.2)
+
+
+@pytest.mark.parametrize("E", [4, 16])
+def test_entry_scores_are_token_scores_with_entry_masks(E):
+    """Entry scores equal token-granularity scores over the same key rows
+    (under a history so long that every row is a candidate), with exactly the
+    entries whose tokens have all arrived kept and the rest -inf."""
+    M, N = 203, 37
+    wl = make_workload(hist_len=[M], new_len=[N], H=2, d=32, idx_dtype="f32", k=8, seed=E,
+                       entry_shift=int(math.log2(E)), hot=False)
+    C = int(wl.ctx_len[0])
+    assert C == (M + N) // E and wl.kI.shape[0] == C
+    rows = np.arange(N, dtype=np.int32)
+    got = oracle.index_scores(wl.q_start, wl.hist_len, wl.q, "f32", None, wl.kI, "f32", None, wl.w, rows,
+                              entry=E)
+    keys = np.concatenate([wl.kI, np.zeros((N, wl.d), np.float32)])  # rows C.. are never read below
+    every = oracle.index_scores([0, N], [C], wl.q, "f32", None, keys, "f32", None, wl.w, rows)[:, :C]
+    assert got.shape == (N, C)
+    for i in range(N):
+        ok = np.array([_entry_ok(j, E, M + i) for j in range(C)])
+        assert np.array_equal(got[i, ok], every[i, ok])
+        assert np.all(np.isneginf(got[i, ~ok]))
+    # one new entry completes every E appended tokens
+    counts = np.isfinite(got).sum(axis=1)
+    assert counts[0] == (M + 1) // E and counts[-1] == C
+
+
+@pytest.mark.parametrize("E", [4, 16])
+def test_entry_topk_and_sharded_over_entry_candidates(E):
+    M, N, k = 150, 20, 12
+    rng = np.random.default_rng(E)
+    C = (M + N) // E
+    sc = rng.integers(0, 5, size=(N, C)).astype(np.float32)  # many ties
+    rows = np.arange(N, dtype=np.int32)
+    got = oracle.topk([0, N], [M], rows, sc, k, entry=E)
+    for i in range(N):
+        cand = [j for j in range(C) if _entry_ok(j, E, M + i)]
+        order = [cand[t] for t in np.lexsort((np.array(cand), -sc[i, cand]))] if cand else []
+        want = (order + [-1] * k)[:k]
+        assert list(got[i]) == want
+    # sharded: only the entries wholly in the history are candidates
+    G, align = 2, 4
+    gs = oracle.topk_sharded([0, N], [M], rows, sc, k, G, align, entry=E)
+    hist = [j for j in range(C) if _entry_ok(j, E, M - 1)]
+    units = -(-len(hist) // align)
+    L = align * (-(-units // G))
+    for i in range(N):
+        for n in range(G):
+            part = [j for j in hist if n * L <= j < (n + 1) * L]
+            order = [part[t] for t in np.lexsort((np.array(part), -sc[i, part]))] if part else []
+            assert list(gs[i, n * (k // G):(n + 1) * (k // G)]) == (order + [-1] * (k // G))[:k // G]
+
+
+def test_entry_page_demand_keeps_history_entries_only():
+    E, M, N, ps = 8, 100, 30, 4
+    C = (M + N) // E
+    rng = np.random.default_rng(3)
+    sel = rng.integers(-1, C + 2, size=(N, 6)).astype(np.int32)
+    pt = rng.permutation(8).astype(np.int32).reshape(1, 8)
+    bm, lst, cnt = oracle.page_demand([0, N], [M], sel, pt, ps, 8, entry=E)
+    want = sorted({int(pt[0, s // ps]) for s in sel.reshape(-1) if 0 <= s < C and _entry_ok(s, E, M - 1)})
+    assert list(lst) == want and cnt == len(want)
+
+
+@pytest.mark.parametrize("E", [2, 8])
+def test_entry_attention_equals_token_attention_with_entry_masks(E):
+    """Attention over entries equals token-granularity attention over the
+    same rows (every id a candidate) after the not-yet-complete entries are
+    turned into padding."""
+    M, N = 90, 21
+    wl = make_workload(hist_len=[M], new_len=[N], H=2, d=32, idx_dtype="f32", k=10, page_size=4, seed=E,
+                       entry_shift=int(math.log2(E)), attn=SMALL_MQA)
+    ai = attention_inputs(wl)
+    sel = synth_topk(wl, seed=1)
+    C = int(wl.ctx_len[0])
+    rng = np.random.default_rng(E)
+    sel[:, :3] = rng.integers(0, C, size=(N, 3))  # some ids past each token's entries
+    rows = np.arange(N, dtype=np.int32)
+    args = (ai.k_pool.reshape(-1, ai.dqk), ai.v_pool.reshape(-1, ai.dv), ai.dqk, ai.dv, wl.page_table,
+            wl.page_size)
+    o1, l1 = oracle.sparse_attn(wl.q_start, wl.hist_len, rows, ai.q, *args, sel, ai.scale, ai.dv, entry=E)
+    masked = np.array([[s if 0 <= s < C and _entry_ok(int(s), E, M + i) else -1 for s in sel[i]]
+                       for i in range(N)], dtype=np.int32)
+    o2, l2 = oracle.sparse_attn([0, N], [C], rows, ai.q, *args, masked, ai.scale, ai.dv)
+    assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
+    assert np.any(masked != sel)

@@ -159,6 +159,7 @@ class Workload:
     q_pred: Optional[np.ndarray] = None
     q_pred_scale: Optional[np.ndarray] = None
     k_bscale: Optional[np.ndarray] = None   # MXFP4 keys: E8M0 [total_ctx, d/32]; kI is then [total_ctx, d/2]
+    entry_shift: int = 0     # ids are entries of 2^entry_shift tokens (0: tokens)
 
     # ---- derived batch description -------------------------------------
     @property
@@ -167,7 +168,13 @@ class Workload:
 
     @property
     def ctx_len(self) -> np.ndarray:
-        return (self.hist_len + self.new_len).astype(np.int32)
+        """Ids (key rows, score row length) per session: tokens, or whole entries."""
+        return ((self.hist_len + self.new_len) >> self.entry_shift).astype(np.int32)
+
+    @property
+    def hist_ids(self) -> np.ndarray:
+        """History ids per session: tokens, or entries wholly in the history."""
+        return (self.hist_len >> self.entry_shift).astype(np.int32)
 
     @property
     def q_start(self) -> np.ndarray:
@@ -221,8 +228,12 @@ def _hot_spans(rng: np.random.Generator, M: int, n_spans: int = 8, frac: float =
 
 def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_run=32,
                   seed=0, layer=0, w_scale=1.0, hot=True, table="identity",
-                  attn=None, q_pred_corr=None, name="custom", key_format=None) -> Workload:
+                  attn=None, q_pred_corr=None, name="custom", key_format=None, entry_shift=0) -> Workload:
     """Build one layer's indexer inputs for a (possibly ragged) batch of sessions.
+
+    With ``entry_shift`` = e > 0 the keys, hot spans, pages and KV rows are
+    per entry of 2^e tokens: session b has (M_b + N_b) >> e of them, the first
+    M_b >> e from the history.  Queries stay per token.
 
     ``table`` is "identity" (logical page p of session b -> physical page
     base_b + p) or "permuted" (one seeded permutation of the pool, sliced
@@ -232,7 +243,8 @@ def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_ru
     hist_len = np.asarray(hist_len, dtype=np.int32).reshape(-1)
     new_len = np.asarray(new_len, dtype=np.int32).reshape(-1)
     B = hist_len.shape[0]
-    ctx = hist_len + new_len
+    ctx = (hist_len + new_len) >> entry_shift   # ids per session
+    hist_ids = hist_len >> entry_shift
     pages_per = (ctx + page_size - 1) // page_size
     num_phys = int(pages_per.sum())
     pt_ld = int(max(1, pages_per.max()))
@@ -240,15 +252,15 @@ def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_ru
     # 1. hot spans (layer independent: the same positions in every layer)
     spans = []
     for b in range(B):
-        spans.append(_hot_spans(_rng(seed, S_HOT, b), int(hist_len[b])) if hot else [])
+        spans.append(_hot_spans(_rng(seed, S_HOT, b), int(hist_ids[b])) if hot else [])
 
     # 2./3. indexer keys, history then new tokens, per session
     keys = []
     for b in range(B):
-        kh = _rng(seed, S_KHIST, layer, b).standard_normal((int(hist_len[b]), d), dtype=np.float32)
+        kh = _rng(seed, S_KHIST, layer, b).standard_normal((int(hist_ids[b]), d), dtype=np.float32)
         for (s0, ln) in spans[b]:
             kh[s0:s0 + ln] *= np.float32(3.0)
-        kn = _rng(seed, S_KNEW, layer, b).standard_normal((int(new_len[b]), d), dtype=np.float32)
+        kn = _rng(seed, S_KNEW, layer, b).standard_normal((int(ctx[b] - hist_ids[b]), d), dtype=np.float32)
         keys.append(kh)
         keys.append(kn)
     kI_f = np.concatenate(keys, axis=0) if keys else np.zeros((0, d), np.float32)
@@ -293,7 +305,7 @@ def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_ru
                     H=H, d=d, idx_dtype=idx_dtype, q=q, q_scale=q_scale, kI=kI, k_scale=k_scale,
                     w=w, k=k, page_size=page_size, max_run=max_run, page_table=pt,
                     num_phys_pages=num_phys, hot_spans=spans, attn_cfg=dict(attn or {}),
-                    q_pred=q_pred, q_pred_scale=q_pred_scale, k_bscale=k_bscale)
+                    q_pred=q_pred, q_pred_scale=q_pred_scale, k_bscale=k_bscale, entry_shift=int(entry_shift))
 
 
 MLA_ATTN = dict(Hq=128, dqk=576, dv=512, mla=True, q_std=1.0, kv_std=1.0 / math.sqrt(576.0),
@@ -413,7 +425,8 @@ def attention_inputs(wl: Workload, with_q: bool = True) -> AttnInputs:
 def synth_topk(wl: Workload, seed: int = 0, hot_frac: float = 0.6, pad_rows: int = 0) -> np.ndarray:
     """Selections shaped like real ones, without scoring anything.
 
-    Row i of session b gets min(k, M_b + i + 1) distinct ids in [0, M_b + i]:
+    Row i of session b gets min(k, n) distinct ids in [0, n), n = M_b + i + 1
+    (entries: (M_b + i + 1) >> entry_shift):
     a hot_frac share drawn from the session's hot spans, the rest uniformly,
     in random order, padded with -1.  The last ``pad_rows`` rows of each
     session also get a few -1 holes and out-of-range ids in place of real ones.
@@ -426,7 +439,9 @@ def synth_topk(wl: Workload, seed: int = 0, hot_frac: float = 0.6, pad_rows: int
         M = int(wl.hist_len[b])
         hot = np.concatenate([np.arange(s, s + n) for (s, n) in wl.hot_spans[b]]) if wl.hot_spans[b] else np.zeros(0, np.int64)
         for i in range(int(wl.new_len[b])):
-            n = M + i + 1
+            n = (M + i + 1) >> wl.entry_shift  # ids that exist at this token
+            if n == 0:
+                continue
             want = min(k, n)
             nh = min(int(hot_frac * want), hot.shape[0])
             sel = rng.choice(hot, nh, replace=False) if nh else np.zeros(0, np.int64)
