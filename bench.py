@@ -158,6 +158,9 @@ def main():
     counts = diff_out[2].cpu().tolist()
     sharded = sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, pd_out[0], pt, ps, P, mr, k)
     decode = decode_step(janus, torch, max(args.steps, 5)) if not args.no_decode else None
+    share = indexshare_group(janus, torch, step_calls=(bt, q, kI, w, sq, sk, pt, ps, P, mr, k, scores, sel, qa, kv,
+                                                       pd_out, diff_out, pred_bm, out, lse, ai),
+                             steps=max(args.steps, 3))
     rec = {
         "metric": "new tokens/s per layer (indexer+top-k+sparse attn) at 128K history; % MFMA/HBM peak",
         "value": N * args.steps / wall,
@@ -190,6 +193,7 @@ def main():
         "demand": {"pages": int(pd_out[3][0]), "runs": int(pd_out[3][1]), "pred_counts": counts},
         "sharded_prediction": sharded,
         "decode": decode,
+        "indexshare": share,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows)
@@ -274,6 +278,45 @@ def sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, actual_bm, 
         res[str(G)] = {"topk_ms": e0.elapsed_time(e1), "recall": ap / a if a else 1.0,
                        "precision": ap / p if p else 1.0, "pred_pages": p, "miss_pages": c[3]}
     return res
+
+
+def indexshare_group(janus, torch, step_calls, steps):
+    """IndexShare (GLM-5 series, Sec. 2.1): four consecutive sparse-attention
+    layers share one selection, and only the first runs the indexer and top-k.
+    One group at the 128K workload: scores -> top-k -> page demand ->
+    corrective set (once: the four layers' KV pools share the page table, so
+    their page sets coincide) -> attention of four layers, each over its own
+    queries and KV pool (layers 1-3 drawn on the GPU from a seeded generator)
+    with the shared ids.  Reported per layer: the group's time over four."""
+    (bt, q, kI, w, sq, sk, pt, ps, P, mr, k, scores, sel, qa, kv, pd_out, diff_out, pred_bm, out, lse, ai) = step_calls
+    dev = qa.device
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    layers = [(qa, kv)]
+    for _ in range(3):
+        layers.append((torch.randn(qa.shape, generator=g, device=dev).to(torch.bfloat16),
+                       (torch.randn(kv.shape, generator=g, device=dev) / 24.0).to(torch.bfloat16)))
+
+    def group():
+        janus.index_scores(bt, q, kI, w, q_scale=sq, k_scale=sk, scores=scores)
+        janus.topk(bt, scores, k, out=sel)
+        janus.page_demand(bt, sel, pt, ps, P, mr, out=pd_out)
+        janus.predict_diff(pd_out[0], pred_bm, P, mr, out=diff_out)
+        for ql, kvl in layers:
+            janus.sparse_attn(bt, ql, kvl, kvl, pt, ps, sel, ai.scale, dv=ai.dv, out=out, lse=lse)
+
+    group()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        group()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) / steps * 1e3
+    del layers
+    N = bt.total_q
+    return {"workload": "4 sparse layers sharing one selection (IndexShare) at the 128K workload",
+            "layers": 4, "ms_per_group": ms, "ms_per_layer": ms / 4,
+            "value": N / (ms / 4) * 1e3, "unit": "new tokens/s per layer"}
 
 
 def decode_step(janus, torch, steps):
