@@ -158,6 +158,7 @@ def main():
     counts = diff_out[2].cpu().tolist()
     sharded = sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, pd_out[0], pt, ps, P, mr, k)
     decode = decode_step(janus, torch, max(args.steps, 5)) if not args.no_decode else None
+    kv8 = fp8kv_attention(janus, torch, bt, qa, kv, pt, ps, sel, ai, max(args.steps, 5), per["sparse_attn"])
     share = indexshare_group(janus, torch, step_calls=(bt, q, kI, w, sq, sk, pt, ps, P, mr, k, scores, sel, qa, kv,
                                                        pd_out, diff_out, pred_bm, out, lse, ai),
                              steps=max(args.steps, 3))
@@ -194,6 +195,7 @@ def main():
         "sharded_prediction": sharded,
         "decode": decode,
         "indexshare": share,
+        "fp8_kv": kv8,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows)
@@ -278,6 +280,36 @@ def sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, actual_bm, 
         res[str(G)] = {"topk_ms": e0.elapsed_time(e1), "recall": ap / a if a else 1.0,
                        "precision": ap / p if p else 1.0, "pred_pages": p, "miss_pages": c[3]}
     return res
+
+
+def fp8kv_attention(janus, torch, bt, qa, kv, pt, ps, sel, ai, steps, bf16_ms):
+    """Attention of the 128K workload over the KV cache kept in FP8 (Sec. 5.1):
+    the bf16 pool quantised on the GPU, one fp32 scale per row (amax/448),
+    rows of 576 e4m3 bytes + the scale, 592 bytes.  Same queries and ids."""
+    rows = kv.shape[0] * kv.shape[1]
+    x = kv.reshape(rows, -1).float()
+    scale = (x.abs().amax(dim=1).clamp_min(1e-12) / 448.0).float()
+    pool8 = torch.zeros((rows, 592), dtype=torch.uint8, device=kv.device)
+    pool8[:, :576] = (x / scale[:, None]).to(torch.float8_e4m3fn).view(torch.uint8)
+    pool8[:, 576:580] = scale.view(torch.uint8).reshape(rows, 4)
+    del x
+    out = torch.empty((bt.total_q, ai.Hq, ai.dv), dtype=torch.bfloat16, device=kv.device)
+    ws = torch.empty(1, dtype=torch.uint8, device=kv.device)
+    f = lambda: janus.sparse_attn_fp8kv(bt, qa, pool8, pt, ps, sel, ai.scale, out=out, workspace=ws)
+    f()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        f()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    gather = bt.total_q * sel.shape[1] * 592.0
+    return {"workload": "sparse attention of the 128K workload over fp8 KV rows (576 e4m3 + fp32 scale)",
+            "ms": ms, "bf16_ms": bf16_ms, "speedup_vs_bf16": bf16_ms / ms,
+            "gather_GBps_logical": gather / (ms * 1e-3) / 1e9,
+            "gather_frac_hbm": gather / (ms * 1e-3) / PEAK_HBM}
 
 
 def indexshare_group(janus, torch, step_calls, steps):

@@ -15,6 +15,7 @@
  *   janus_sparse_attn   attention over the selected tokens only      (after Eq. 1)
  *   janus_sparse_attn_split  the same with each row's selection split over
  *                       several blocks, for few rows (decode, Sec. 2.2)
+ *   janus_sparse_attn_fp8kv  MLA attention over an FP8 KV cache (Sec. 5.1)
  *
  * Running index_scores + topk + page_demand on a predicted indexer query
  * (an earlier layer's hidden state through this layer's indexer) gives the
@@ -294,6 +295,38 @@ int janus_sparse_attn_split(const janus_batch *b,
                             const void *q, int Hq, int dqk, int dv,
                             const void *k_pool, const void *v_pool,
                             int64_t k_row_stride, int64_t v_row_stride,
+                            const int32_t *page_table, int pt_ld, int page_size,
+                            const int32_t *topk_idx, int k, float softmax_scale,
+                            void *out, janus_dtype out_dt, float *lse,
+                            int num_splits, void *workspace, size_t *workspace_bytes,
+                            void *stream);
+
+/*
+ * Sparse MLA attention over a KV cache stored in FP8 (Sec. 5.1 keeps KV
+ * states in FP8).  The same attention as janus_sparse_attn with dqk = 576
+ * and dv = 512, where every cached row is
+ *
+ *   bytes 0..575    the 576 latent+rope elements, OCP fp8 e4m3fn
+ *   bytes 576..579  the row's fp32 scale (> 0, finite)
+ *   bytes 580..     unused, up to row_bytes
+ *
+ * and stands for the values scale * e4m3(byte): K_s is the whole row, V_s its
+ * first 512 elements.  The row of id s is pool row
+ * page_table[b, s/page_size]*page_size + s%page_size, at kv_pool + that * row_bytes.
+ *   q        device [total_q, Hq, 576] bf16, 16-byte aligned; Hq in {16, 32, 64, 128}
+ *   kv_pool  device, 16-byte aligned; row_bytes >= 592 and a multiple of 16
+ *   k        <= 4096
+ *   out, lse, num_splits, workspace, workspace_bytes: as janus_sparse_attn_split
+ *            (num_splits = 1 runs unsplit and needs no workspace)
+ * The stored values are exact in bf16: products run on bf16 MFMA, softmax and
+ * accumulation in fp32.  Each key's scale multiplies its logit and, before the
+ * bf16 rounding of the probabilities, its probability.  Shapes outside the
+ * above return JANUS_ERR_UNSUPPORTED (alignment, Hq, k) or
+ * JANUS_ERR_INVALID_ARG (row_bytes < 592, NULL pointers).
+ */
+int janus_sparse_attn_fp8kv(const janus_batch *b,
+                            const void *q, int Hq,
+                            const uint8_t *kv_pool, int64_t row_bytes,
                             const int32_t *page_table, int pt_ld, int page_size,
                             const int32_t *topk_idx, int k, float softmax_scale,
                             void *out, janus_dtype out_dt, float *lse,

@@ -60,7 +60,8 @@ def lib():
         L.jo_predict_diff.argtypes = [P, P, i32, i32, P, P, P]
         L.jo_sparse_attn.argtypes = [i32, P, P, i32, i32, P, P, i32, i32, i32, P, P, i64, i64,
                                      P, i32, i32, P, i32, dbl, P, P]
-        for f in ("jo_index_scores", "jo_topk", "jo_topk_sharded", "jo_page_demand", "jo_runs",
+        L.jo_sparse_attn_fp8kv.argtypes = [i32, P, P, i32, i32, P, P, i32, P, i64, P, i32, i32, P, i32, dbl, P, P]
+        for f in ("jo_index_scores", "jo_sparse_attn_fp8kv", "jo_topk", "jo_topk_sharded", "jo_page_demand", "jo_runs",
                   "jo_predict_diff", "jo_sparse_attn"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
@@ -223,4 +224,25 @@ def sparse_attn(q_start, hist_len, rows, q_rows, k_pool, v_pool, k_row_stride, v
                               _p(kp), _p(vp), k_row_stride, v_row_stride, _p(pt), pt.shape[1], page_size,
                               _p(sel), sel.shape[1], float(scale), _p(out), _p(lse))
     _check(rc, "sparse_attn")
+    return out, lse
+
+
+def sparse_attn_fp8kv(q_start, hist_len, rows, q_rows, kv_pool, page_table, page_size, sel_rows, scale, entry=1):
+    """MLA attention (float64) over fp8 KV rows: kv_pool uint8 [..., row_bytes],
+    576 e4m3 bytes then the fp32 scale.  Returns (out [n, Hq, 512], lse [n, Hq])."""
+    q_start = _c(q_start, np.int32)
+    hist_len = _c(hist_len, np.int32)
+    rows = _c(rows, np.int32)
+    q_rows = _c(q_rows, np.uint16)
+    n, Hq, _ = q_rows.shape
+    kv = _c(kv_pool, np.uint8)
+    row_bytes = kv.shape[-1]
+    out = np.empty((n, Hq, 512), dtype=np.float64)
+    lse = np.empty((n, Hq), dtype=np.float64)
+    pt = _c(page_table, np.int32)
+    sel = _c(sel_rows, np.int32)
+    rc = lib().jo_sparse_attn_fp8kv(len(hist_len), _p(q_start), _p(hist_len), entry, n, _p(rows), _p(q_rows), Hq,
+                                    _p(kv), row_bytes, _p(pt), pt.shape[1], page_size, _p(sel), sel.shape[1],
+                                    float(scale), _p(out), _p(lse))
+    _check(rc, "sparse_attn_fp8kv")
     return out, lse

@@ -33,7 +33,9 @@
  *     read packing".  Runs are additionally split from their low end into
  *     pieces of at most max_run pages.
  *   - sparse attention over the selected tokens only: the paragraph after
- *     Eq. (1) (KV of the selected tokens feed core attention).
+ *     Eq. (1) (KV of the selected tokens feed core attention); KV states kept
+ *     in FP8 (Sec. "Experiments", models), read as e4m3 with one fp32 scale
+ *     per cached row.
  *   - entry granularity (Sec. "Sparse Attention", footnote on DeepSeek-V4;
  *     the notation table applies unchanged): a candidate is an entry, one
  *     cached row standing for E consecutive tokens, E*j .. E*j + E - 1, which
@@ -483,6 +485,15 @@ int jo_predict_diff(const uint32_t *actual, const uint32_t *predicted, int num_p
  * lse [nrows, Hq] (may be NULL): log-sum-exp of the scaled logits.
  * A row with no valid id gives out = 0 and lse = -inf.
  */
+static int sparse_attn_impl(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
+                            int nrows, const int32_t *rows,
+                            const uint16_t *q, int Hq, int dqk, int dv,
+                            const void *k_pool, const void *v_pool,
+                            int64_t k_row_stride, int64_t v_row_stride, int kv_fp8,
+                            const int32_t *page_table, int pt_ld, int page_size,
+                            const int32_t *sel, int k, double scale,
+                            double *out, double *lse);
+
 int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
                    int nrows, const int32_t *rows,
                    const uint16_t *q, int Hq, int dqk, int dv,
@@ -491,6 +502,52 @@ int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len, in
                    const int32_t *page_table, int pt_ld, int page_size,
                    const int32_t *sel, int k, double scale,
                    double *out, double *lse)
+{
+    return sparse_attn_impl(nseq, q_start, hist_len, E, nrows, rows, q, Hq, dqk, dv, k_pool, v_pool, k_row_stride,
+                            v_row_stride, 0, page_table, pt_ld, page_size, sel, k, scale, out, lse);
+}
+
+/*
+ * The same attention over a KV cache kept in FP8 (Sec. "Experiments",
+ * models: KV states are stored in FP8).  MLA layout: a pool row of row_bytes
+ * bytes holds 576 e4m3 elements, then the row's fp32 scale at byte 576; it
+ * stands for scale * e4m3(byte).  K_s is the whole row, V_s its first 512
+ * elements; q [nrows, Hq, 576] bf16, out [nrows, Hq, 512].
+ */
+int jo_sparse_attn_fp8kv(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
+                         int nrows, const int32_t *rows,
+                         const uint16_t *q, int Hq,
+                         const uint8_t *kv_pool, int64_t row_bytes,
+                         const int32_t *page_table, int pt_ld, int page_size,
+                         const int32_t *sel, int k, double scale,
+                         double *out, double *lse)
+{
+    if (row_bytes < 580)
+        return -1;
+    return sparse_attn_impl(nseq, q_start, hist_len, E, nrows, rows, q, Hq, 576, 512, kv_pool, kv_pool, row_bytes,
+                            row_bytes, 1, page_table, pt_ld, page_size, sel, k, scale, out, lse);
+}
+
+/* Element e of pool row `row`: bf16 (row stride in elements), or fp8 e4m3
+ * times the fp32 scale stored after the row's 576 elements (stride in bytes). */
+static double kv_elem(const void *pool, int64_t row, int64_t stride, int kv_fp8, int e)
+{
+    if (!kv_fp8)
+        return jo_bf16_value(((const uint16_t *)pool)[row * stride + e]);
+    const uint8_t *rp = (const uint8_t *)pool + row * stride;
+    float sc;
+    memcpy(&sc, rp + 576, sizeof sc);
+    return jo_fp8_e4m3fn_value(rp[e]) * (double)sc;
+}
+
+static int sparse_attn_impl(int nseq, const int32_t *q_start, const int32_t *hist_len, int E,
+                            int nrows, const int32_t *rows,
+                            const uint16_t *q, int Hq, int dqk, int dv,
+                            const void *k_pool, const void *v_pool,
+                            int64_t k_row_stride, int64_t v_row_stride, int kv_fp8,
+                            const int32_t *page_table, int pt_ld, int page_size,
+                            const int32_t *sel, int k, double scale,
+                            double *out, double *lse)
 {
     if (nseq < 1 || Hq < 1 || dqk < 1 || dv < 1 || k < 1 || page_size < 1 || nrows < 0 || E < 1)
         return -1;
@@ -519,8 +576,8 @@ int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len, in
             }
             int64_t phys = page_table[(int64_t)b * pt_ld + lp];
             int64_t slot = phys * page_size + s % page_size;
-            krow[nv] = slot * k_row_stride;
-            vrow[nv] = slot * v_row_stride;
+            krow[nv] = slot;
+            vrow[nv] = slot;
             nv++;
         }
         for (int h = 0; h < Hq; h++) {
@@ -537,7 +594,7 @@ int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len, in
             for (int j = 0; j < nv; j++) {
                 double x = 0.0;
                 for (int e = 0; e < dqk; e++)
-                    x += jo_bf16_value(qh[e]) * jo_bf16_value(k_pool[krow[j] + e]);
+                    x += jo_bf16_value(qh[e]) * kv_elem(k_pool, krow[j], k_row_stride, kv_fp8, e);
                 logit[j] = scale * x;
                 if (logit[j] > m)
                     m = logit[j];
@@ -547,7 +604,7 @@ int jo_sparse_attn(int nseq, const int32_t *q_start, const int32_t *hist_len, in
                 double p = exp(logit[j] - m);
                 denom += p;
                 for (int e = 0; e < dv; e++)
-                    o[e] += p * jo_bf16_value(v_pool[vrow[j] + e]);
+                    o[e] += p * kv_elem(v_pool, vrow[j], v_row_stride, kv_fp8, e);
             }
             for (int e = 0; e < dv; e++)
                 o[e] /= denom;

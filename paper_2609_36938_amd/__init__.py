@@ -64,8 +64,10 @@ def lib():
         L.janus_index_scores_mxfp4.argtypes = [BP, P, P, P, P, P, P, i32, i32, P, P]
         L.janus_sparse_attn_split.argtypes = [BP, P, i32, i32, i32, P, P, i64, i64, P, i32, i32, P, i32, f32, P,
                                               i32, P, i32, P, SZ, P]
+        L.janus_sparse_attn_fp8kv.argtypes = [BP, P, i32, P, i64, P, i32, i32, P, i32, f32, P, i32, P, i32, P, SZ, P]
         for f in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
-                  "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split", "janus_index_scores_mxfp4"):
+                  "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split", "janus_index_scores_mxfp4",
+                  "janus_sparse_attn_fp8kv"):
             getattr(L, f).restype = ctypes.c_int
         L.janus_status_string.argtypes = [ctypes.c_int]
         L.janus_status_string.restype = ctypes.c_char_p
@@ -274,4 +276,30 @@ def sparse_attn_split(batch: Batch, q, k_pool, v_pool, page_table, page_size: in
     have = ctypes.c_size_t(workspace.numel() * workspace.element_size())
     rc = lib().janus_sparse_attn_split(*args, _ptr(workspace), ctypes.byref(have), _stream(stream))
     _check(rc, "janus_sparse_attn_split")
+    return out, lse
+
+
+def sparse_attn_fp8kv(batch: Batch, q, kv_pool, page_table, page_size: int, topk_idx, scale: float,
+                      num_splits: int = 1, out_dtype: str = "bf16", want_lse: bool = False, out=None, lse=None,
+                      workspace=None, stream=None):
+    """janus_sparse_attn_fp8kv: MLA attention (576/512) over fp8 KV rows
+    (uint8 [..., row_bytes]: 576 e4m3 bytes, the fp32 scale at byte 576);
+    num_splits as for sparse_attn_split (1: unsplit).  Returns (out, lse or None)."""
+    Hq = int(q.shape[-2])
+    row_bytes = int(kv_pool.shape[-1])
+    odt = {"bf16": (JANUS_BF16, torch.bfloat16), "f32": (JANUS_F32, torch.float32)}[out_dtype]
+    if out is None:
+        out = torch.empty((batch.total_q, Hq, 512), dtype=odt[1], device=q.device)
+    if want_lse and lse is None:
+        lse = torch.empty((batch.total_q, Hq), dtype=torch.float32, device=q.device)
+    args = (batch.ref, _ptr(q), Hq, _ptr(kv_pool), row_bytes, _ptr(page_table), int(page_table.shape[1]),
+            int(page_size), _ptr(topk_idx), int(topk_idx.shape[1]), float(scale), _ptr(out), odt[0], _ptr(lse),
+            int(num_splits))
+    need = ctypes.c_size_t(0)
+    _check(lib().janus_sparse_attn_fp8kv(*args, None, ctypes.byref(need), _stream(stream)), "janus_sparse_attn_fp8kv")
+    if workspace is None:
+        workspace = torch.empty(max(int(need.value), 1), dtype=torch.uint8, device=q.device)
+    have = ctypes.c_size_t(workspace.numel() * workspace.element_size())
+    rc = lib().janus_sparse_attn_fp8kv(*args, _ptr(workspace), ctypes.byref(have), _stream(stream))
+    _check(rc, "janus_sparse_attn_fp8kv")
     return out, lse

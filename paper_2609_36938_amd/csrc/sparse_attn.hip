@@ -76,23 +76,75 @@ JANUS_DEV v4s16 lds_read_tr16(const uint8_t *lds_base, int byte_off)
 // Every wave issues the same number of gather instructions per tile, so a
 // counted wait is exact; instruction slots past the tile's chunks load a
 // dummy chunk into padding.
-template <int NW>
-constexpr int mla_ipw() { return (MLA_TILE_INS + NW - 1) / NW; }
-template <int NW>
-constexpr int mla_buf_bytes() { return NW * mla_ipw<NW>() * 64 * 16; }
+// fp8 KV rows: 576 e4m3 bytes, the row's fp32 scale at byte 576, padding to
+// 592 bytes (37 chunks, all gathered).  A tile keeps that pitch in LDS, with
+// keys 16..31 a further 128 bytes on: the K reads (keys c16 and c16+16, in
+// separate instructions) and the transposing V reads (keys 4g+j and
+// 16+4g+j, together) then each touch distinct 16-byte bank groups.
+constexpr int KV8_ROWB = 592;
+constexpr int KV8_CPR = KV8_ROWB / 16;                   // 37
+constexpr int KV8_GAP = 8;                               // chunks between keys 15 and 16
+constexpr int KV8_TILE_CH = MLA_KT * KV8_CPR + KV8_GAP;  // 1192
+constexpr int KV8_SCALE = MLA_DQK;                       // byte of the scale in a row
+JANUS_DEV int kv8_key_off(int r) { return r * KV8_ROWB + (r >= 16 ? KV8_GAP * 16 : 0); }
 
-template <int NW, bool SPLIT>
+template <bool KV8>
+constexpr int mla_tile_ch() { return KV8 ? KV8_TILE_CH : MLA_TILE_CH; }
+template <int NW, bool KV8>
+constexpr int mla_ipw() { return ((mla_tile_ch<KV8>() + 63) / 64 + NW - 1) / NW; }
+template <int NW, bool KV8>
+constexpr int mla_buf_bytes() { return NW * mla_ipw<NW, KV8>() * 64 * 16; }
+
+// Tile chunk qch -> key row r and chunk c of that row.  Chunks that are not
+// part of a row (row padding, the fp8 gap) load chunk 0 of key r: a dummy.
+template <bool KV8>
+JANUS_DEV void tile_chunk(int qch, int &r, int &c)
+{
+    if constexpr (KV8) {
+        const bool hi = qch >= 16 * KV8_CPR;
+        const int q2 = hi ? qch - 16 * KV8_CPR - KV8_GAP : qch;
+        const int rr = q2 < 0 ? 0 : q2 / KV8_CPR;
+        r = rr + (hi ? 16 : 0);
+        c = q2 < 0 ? 0 : q2 - rr * KV8_CPR;
+    } else {
+        r = qch / MLA_PCH;
+        c = qch - r * MLA_PCH;
+        if (c >= MLA_CPR)
+            c = 0;
+    }
+}
+
+// 8 fp8 e4m3 values -> 8 bf16 (exact: e4m3 values are bf16 values)
+JANUS_DEV v8bf fp8x8_to_bf16(v2i x)
+{
+    const v2bf a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[0], 1.0f, false);
+    const v2bf b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[0], 1.0f, true);
+    const v2bf c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[1], 1.0f, false);
+    const v2bf d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[1], 1.0f, true);
+    return v8bf{a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
+}
+
+// Transposing LDS read of bytes (ds_read_b64_tr_b8): within each 16-lane
+// group, lane i's byte j is byte i%8 of the 8 bytes addressed by lane 2j+i/8.
+JANUS_DEV v2i lds_read_tr8(const uint8_t *lds_base, int byte_off)
+{
+    return __builtin_amdgcn_ds_read_tr8_b64_v2i32(
+        (__attribute__((address_space(3))) v2i *)((__attribute__((address_space(3))) uint8_t *)lds_base + byte_off));
+}
+
+template <int NW, bool SPLIT, bool KV8>
 __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs, int es,
-    const uint16_t *__restrict__ q, const uint16_t *__restrict__ kv, int64_t row_stride,
+    const uint16_t *__restrict__ q, const uint8_t *__restrict__ kv, int64_t row_bytes,
     const int32_t *__restrict__ page_table, int pt_ld, int page_shift, const int32_t *__restrict__ topk,
     int k, float scale_log2, void *__restrict__ out, int out_f32, float *__restrict__ lse, int num_splits,
     float *__restrict__ part)
 {
     constexpr int HQ = 16 * NW;  // one 16-head MFMA block per wave for S and P
     constexpr int NT = 64 * NW;
-    constexpr int IPW = mla_ipw<NW>();
-    constexpr int BUF = mla_buf_bytes<NW>();
+    constexpr int IPW = mla_ipw<NW, KV8>();
+    constexpr int BUF = mla_buf_bytes<NW, KV8>();
+    constexpr int TILE_CH = mla_tile_ch<KV8>();
     // three tile buffers; tile_step's restrict-qualified pointers let the
     // compiler see that reading one never waits for the gather into another
     __shared__ __attribute__((aligned(16))) uint8_t sKV0[BUF];
@@ -158,15 +210,13 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         for (int i = i0; i < i1; ++i) {
             const int j = wave + NW * i;
             const int qch = 64 * j + lane;
-            const int r = qch / MLA_PCH;
-            int c = qch - r * MLA_PCH;
-            if (c >= MLA_CPR)
-                c = 0;
+            int r, c;
+            tile_chunk<KV8>(qch, r, c);
             const int key = MLA_KT * t + r;
-            int slot = (qch < MLA_TILE_CH && key < kl) ? sSlot[key] : -1;
+            int slot = (qch < TILE_CH && key < kl) ? sSlot[key] : -1;
             if (slot < 0)
                 slot = 0;  // padding rows read a real row; their logits are masked
-            const uint16_t *src = kv + (int64_t)slot * row_stride + 8 * c;
+            const uint8_t *src = kv + (int64_t)slot * row_bytes + 16 * c;
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
         }
     };
@@ -181,17 +231,17 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
 #pragma unroll
         for (int u = 0; u < NG; ++u) {
             const int qch = 64 * (wave + NW * (I0 + u)) + ln;
-            const int r = qch / MLA_PCH;
-            const int c = qch - r * MLA_PCH;
+            int r, c;
+            tile_chunk<KV8>(qch, r, c);
             const int key = MLA_KT * t + r;
-            slot[u] = (qch < MLA_TILE_CH && key < kl) ? sSlot[key] : -1;
-            cc[u] = c >= MLA_CPR ? 0 : c;
+            slot[u] = (qch < TILE_CH && key < kl) ? sSlot[key] : -1;
+            cc[u] = c;
         }
 #pragma unroll
         for (int u = 0; u < NG; ++u) {
             const int j = wave + NW * (I0 + u);
             const int sl = slot[u] < 0 ? 0 : slot[u];  // padding rows read a real row; their logits are masked
-            const uint16_t *src = kv + (int64_t)sl * row_stride + 8 * cc[u];
+            const uint8_t *src = kv + (int64_t)sl * row_bytes + 16 * cc[u];
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
         }
     };
@@ -200,16 +250,31 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     // behind the gather queue overlaps MFMAs already in flight instead of
     // holding every wave at the top of the step; other wave counts issue
     // them all at step 0
-    constexpr bool SPREAD = IPW == 5;
+    constexpr bool SPREAD = IPW == 5 || (KV8 && IPW >= 2);
     auto issue_part = [&](int t, int part, uint8_t *__restrict__ dst) {
         if (t + 2 < ntiles) {
             if constexpr (SPREAD) {
                 switch (part) {
-                case 0: issue_group(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{}, t + 2, dst); break;
-                case 1: issue_group(std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, t + 2, dst); break;
-                case 2: issue_group(std::integral_constant<int, 2>{}, std::integral_constant<int, 3>{}, t + 2, dst); break;
-                case 3: issue_group(std::integral_constant<int, 3>{}, std::integral_constant<int, 4>{}, t + 2, dst); break;
-                case 4: issue_group(std::integral_constant<int, 4>{}, std::integral_constant<int, 5>{}, t + 2, dst); break;
+                case 0:
+                    if constexpr (IPW > 0)
+                        issue_group(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{}, t + 2, dst);
+                    break;
+                case 1:
+                    if constexpr (IPW > 1)
+                        issue_group(std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, t + 2, dst);
+                    break;
+                case 2:
+                    if constexpr (IPW > 2)
+                        issue_group(std::integral_constant<int, 2>{}, std::integral_constant<int, 3>{}, t + 2, dst);
+                    break;
+                case 3:
+                    if constexpr (IPW > 3)
+                        issue_group(std::integral_constant<int, 3>{}, std::integral_constant<int, 4>{}, t + 2, dst);
+                    break;
+                case 4:
+                    if constexpr (IPW > 4)
+                        issue_group(std::integral_constant<int, 4>{}, std::integral_constant<int, 5>{}, t + 2, dst);
+                    break;
                 default: break;
                 }
             } else if (part == 0) {
@@ -220,22 +285,46 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     auto tile_step = [&](int t, const uint8_t *__restrict__ tile, uint8_t *__restrict__ next) {
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
         v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
-        const uint8_t *row0 = tile + c16 * MLA_ROWB + 16 * grp;
-        const uint8_t *row1 = row0 + 16 * MLA_ROWB;
+        if constexpr (KV8) {
+            // fp8 rows: 8 bytes per lane and step, widened to bf16 in registers
+            const uint8_t *row0 = tile + kv8_key_off(c16) + 8 * grp;
+            const uint8_t *row1 = tile + kv8_key_off(c16 + 16) + 8 * grp;
 #pragma unroll
-        for (int step = 0; step < MLA_STEPS; ++step) {
-            const v4i a0 = *(const v4i *)(row0 + 64 * step);
-            const v4i a1 = *(const v4i *)(row1 + 64 * step);
-            st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a0), qf[step], st0, 0, 0, 0);
-            st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a1), qf[step], st1, 0, 0, 0);
-            if (step % 4 == 0)
-                issue_part(t, step / 4, next);
+            for (int step = 0; step < MLA_STEPS; ++step) {
+                const v2i a0 = *(const v2i *)(row0 + 32 * step);
+                const v2i a1 = *(const v2i *)(row1 + 32 * step);
+                st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(a0), qf[step], st0, 0, 0, 0);
+                st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(a1), qf[step], st1, 0, 0, 0);
+                if (step % 4 == 0)
+                    issue_part(t, step / 4, next);
+            }
+        } else {
+            const uint8_t *row0 = tile + c16 * MLA_ROWB + 16 * grp;
+            const uint8_t *row1 = row0 + 16 * MLA_ROWB;
+#pragma unroll
+            for (int step = 0; step < MLA_STEPS; ++step) {
+                const v4i a0 = *(const v4i *)(row0 + 64 * step);
+                const v4i a1 = *(const v4i *)(row1 + 64 * step);
+                st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a0), qf[step], st0, 0, 0, 0);
+                st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a1), qf[step], st1, 0, 0, 0);
+                if (step % 4 == 0)
+                    issue_part(t, step / 4, next);
+            }
         }
         // online softmax (exp2 domain) with lazy rescaling of O.  Valid keys
         // of the tile come as a 32-bit mask (lanes 32-63 repeat 0-31); this
         // lane's keys are 16*kb + 4*grp + i
         const int vkey = MLA_KT * t + (lane & 31);
         const uint32_t vmask = (uint32_t)__ballot(vkey < kl && sSlot[vkey] >= 0) >> (4 * grp);
+        // fp8 rows: each key's scale multiplies its logit and its probability
+        float ks[2][4];
+        if constexpr (KV8) {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    ks[kb][i] = *(const float *)(tile + kv8_key_off(16 * kb + 4 * grp + i) + KV8_SCALE);
+        }
         float x[2][4];
         float mx = -INFINITY;
 #pragma unroll
@@ -243,7 +332,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 const bool ok = (vmask >> (16 * kb + i)) & 1u;
-                x[kb][i] = ok ? (kb ? st1[i] : st0[i]) * scale_log2 : -INFINITY;
+                const float sc = KV8 ? scale_log2 * ks[kb][i] : scale_log2;
+                x[kb][i] = ok ? (kb ? st1[i] : st0[i]) * sc : -INFINITY;
                 mx = fmaxf(mx, x[kb][i]);
             }
         // the running max m is common to a head's four lane groups; it only
@@ -271,6 +361,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             for (int i = 0; i < 4; ++i) {
                 pv[kb][i] = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[kb][i] - m);
                 lsum += pv[kb][i];
+                if constexpr (KV8)  // V_s = scale_s * (stored row); padding keys stay 0
+                    pv[kb][i] = ((vmask >> (16 * kb + i)) & 1u) ? pv[kb][i] * ks[kb][i] : 0.f;
             }
         const v8bf pa = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
                              (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
@@ -282,16 +374,29 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // 16*hb + c16; slots: keys 4*grp + i and 16 + 4*grp + i).  V operand:
         // those keys, lane (r' = c16/4, cc = c16%4) addressing dims
         // 16*nb + 4*cc .. +3 of its key row
-        const int rr0 = 4 * grp + (c16 >> 2), cc = c16 & 3;
-        const uint8_t *vrow0 = tile + rr0 * MLA_ROWB, *vrow1 = vrow0 + 16 * MLA_ROWB;
-        const int voff = 16 * (cc >> 1) + (cc & 1) * 8;
         v8bf bv[NBW];
+        if constexpr (KV8) {
+            // fp8 rows: lane (c16, grp) addresses key j = c16/2 of the P
+            // fragment's order (4*grp + j, then 16 + 4*grp + j - 4), bytes
+            // 8*(c16&1) .. of a 16-dim block; the byte transpose hands it
+            // those 8 keys at dim 16*nb + c16
+            const int j = c16 >> 1;
+            const int vkey8 = j < 4 ? 4 * grp + j : 12 + 4 * grp + j;
+            const uint8_t *vrow = tile + kv8_key_off(vkey8) + 8 * (c16 & 1);
 #pragma unroll
-        for (int nl = 0; nl < NBW; ++nl) {
-            const int nb = NBW * wave + nl;
-            const v4s16 lo = lds_read_tr16(vrow0, voff + 32 * nb);
-            const v4s16 hi = lds_read_tr16(vrow1, voff + 32 * nb);
-            bv[nl] = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+            for (int nl = 0; nl < NBW; ++nl)
+                bv[nl] = fp8x8_to_bf16(lds_read_tr8(vrow, 16 * (NBW * wave + nl)));
+        } else {
+            const int rr0 = 4 * grp + (c16 >> 2), cc = c16 & 3;
+            const uint8_t *vrow0 = tile + rr0 * MLA_ROWB, *vrow1 = vrow0 + 16 * MLA_ROWB;
+            const int voff = 16 * (cc >> 1) + (cc & 1) * 8;
+#pragma unroll
+            for (int nl = 0; nl < NBW; ++nl) {
+                const int nb = NBW * wave + nl;
+                const v4s16 lo = lds_read_tr16(vrow0, voff + 32 * nb);
+                const v4s16 hi = lds_read_tr16(vrow1, voff + 32 * nb);
+                bv[nl] = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+            }
         }
 #pragma unroll
         for (int hb = 0; hb < NW; ++hb) {
@@ -553,37 +658,89 @@ static bool mla_shape(const void *q, int Hq, int dqk, int dv, const void *k_pool
 }
 
 // one launch of the MLA kernel: splits blocks per token, each over one slice
-// of the selection (part = NULL: splits = 1, normalised output)
-static void launch_mla(const janus_batch *bt, const void *q, int Hq, const void *k_pool, int64_t k_row_stride,
+// of the selection (part = NULL: splits = 1, normalised output); pool rows
+// of row_bytes bytes, bf16 or (kv8) fp8 with an inline scale
+template <bool KV8>
+static void launch_mla(const janus_batch *bt, const void *q, int Hq, const void *k_pool, int64_t row_bytes,
                        const int32_t *page_table, int pt_ld, int shift, const int32_t *topk_idx, int k, float sl2,
                        void *out, int of32, float *lse, int splits, float *part, hipStream_t st)
 {
     const auto *qq = (const uint16_t *)q;
-    const auto *kv = (const uint16_t *)k_pool;
+    const auto *kv = (const uint8_t *)k_pool;
     auto launch = [&](auto kern, int nw) {
         hipLaunchKernelGGL(kern, dim3(bt->total_q * splits), dim3(64 * nw), 0, st, bt->q_start, bt->hist_len,
-                           bt->num_seqs, bt->entry_shift, qq, kv, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32,
-                           lse, splits, part);
+                           bt->num_seqs, bt->entry_shift, qq, kv, row_bytes, page_table, pt_ld, shift, topk_idx, k,
+                           sl2, out, of32, lse, splits, part);
     };
     if (part) {
         if (Hq == 128)
-            launch(sparse_mla_mfma<8, true>, 8);
+            launch(sparse_mla_mfma<8, true, KV8>, 8);
         else if (Hq == 64)
-            launch(sparse_mla_mfma<4, true>, 4);
+            launch(sparse_mla_mfma<4, true, KV8>, 4);
         else if (Hq == 32)
-            launch(sparse_mla_mfma<2, true>, 2);
+            launch(sparse_mla_mfma<2, true, KV8>, 2);
         else
-            launch(sparse_mla_mfma<1, true>, 1);
+            launch(sparse_mla_mfma<1, true, KV8>, 1);
     } else {
         if (Hq == 128)
-            launch(sparse_mla_mfma<8, false>, 8);
+            launch(sparse_mla_mfma<8, false, KV8>, 8);
         else if (Hq == 64)
-            launch(sparse_mla_mfma<4, false>, 4);
+            launch(sparse_mla_mfma<4, false, KV8>, 4);
         else if (Hq == 32)
-            launch(sparse_mla_mfma<2, false>, 2);
+            launch(sparse_mla_mfma<2, false, KV8>, 2);
         else
-            launch(sparse_mla_mfma<1, false>, 1);
+            launch(sparse_mla_mfma<1, false, KV8>, 1);
     }
+}
+
+// The MLA kernel over a whole or sliced selection (see janus_sparse_attn_split
+// for the slice count and workspace rules).
+template <bool KV8>
+static int run_mla(const janus_batch *bt, const void *q, int Hq, const void *pool, int64_t row_bytes,
+                   const int32_t *page_table, int pt_ld, int page_size, const int32_t *topk_idx, int k, float scale,
+                   void *out, janus_dtype out_dt, float *lse, int num_splits, void *workspace,
+                   size_t *workspace_bytes, void *stream)
+{
+    // slices: as given, or (0) enough for one block per compute unit (a
+    // block fills a CU's LDS, so more slices only queue a second round), at
+    // most one slice per 32-id tile and MAX_SPLITS
+    int splits = num_splits;
+    if (splits == 0) {
+        int dev = 0, cus = 256;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return JANUS_ERR_DEVICE;
+        const int tq = std::max(bt->total_q, 1);
+        splits = std::min(MAX_SPLITS, std::max(1, (cus + tq - 1) / tq));
+    }
+    splits = std::min(splits, (k + MLA_KT - 1) / MLA_KT);
+    const size_t need =
+        splits > 1 ? (size_t)bt->total_q * splits * Hq * (MLA_DV + 2) * sizeof(float) : (size_t)0;
+    if (!workspace) {
+        *workspace_bytes = need;
+        return JANUS_OK;
+    }
+    if (*workspace_bytes < need)
+        return JANUS_ERR_WORKSPACE;
+    if (bt->total_q == 0)
+        return JANUS_OK;
+    hipStream_t st = as_stream(stream);
+    const int shift = __builtin_ctz((unsigned)page_size);
+    const float sl2 = scale * LOG2E;
+    const int of32 = out_dt == JANUS_F32;
+    if (splits == 1) {
+        launch_mla<KV8>(bt, q, Hq, pool, row_bytes, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32, lse, 1,
+                        nullptr, st);
+        return launch_status();
+    }
+    float *part = static_cast<float *>(workspace);
+    launch_mla<KV8>(bt, q, Hq, pool, row_bytes, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32, lse, splits,
+                    part, st);
+    if (hipGetLastError() != hipSuccess)
+        return JANUS_ERR_DEVICE;
+    hipLaunchKernelGGL(attn_combine, dim3((int64_t)bt->total_q * Hq), dim3(COMBINE_THREADS), 0, st, part, splits, Hq,
+                       MLA_DV, out, of32, lse);
+    return launch_status();
 }
 
 static bool attn_args_ok(const janus_batch *bt, const void *q, int Hq, int dqk, int dv, const void *k_pool,
@@ -614,8 +771,8 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
     const float sl2 = scale * LOG2E;
     const int of32 = out_dt == JANUS_F32;
     if (mla_shape(q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, k)) {
-        launch_mla(bt, q, Hq, k_pool, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32, lse, 1,
-                   nullptr, st);
+        launch_mla<false>(bt, q, Hq, k_pool, 2 * k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32,
+                          lse, 1, nullptr, st);
         return launch_status();
     }
     if (dqk > VEC_MAX_DQK || dv > 4 * VEC_THREADS)
@@ -643,44 +800,26 @@ extern "C" int janus_sparse_attn_split(const janus_batch *bt, const void *q, int
         return JANUS_ERR_UNSUPPORTED;
     if (!mla_shape(q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, k))
         return JANUS_ERR_UNSUPPORTED;
-    // slices: as given, or (0) enough for one block per compute unit (a
-    // block fills a CU's LDS, so more slices only queue a second round), at
-    // most one slice per 32-id tile and MAX_SPLITS
-    int splits = num_splits;
-    if (splits == 0) {
-        int dev = 0, cus = 256;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            return JANUS_ERR_DEVICE;
-        const int tq = std::max(bt->total_q, 1);
-        splits = std::min(MAX_SPLITS, std::max(1, (cus + tq - 1) / tq));
-    }
-    splits = std::min(splits, (k + MLA_KT - 1) / MLA_KT);
-    const size_t need =
-        splits > 1 ? (size_t)bt->total_q * splits * Hq * (MLA_DV + 2) * sizeof(float) : (size_t)0;
-    if (!workspace) {
-        *workspace_bytes = need;
-        return JANUS_OK;
-    }
-    if (*workspace_bytes < need)
-        return JANUS_ERR_WORKSPACE;
-    if (bt->total_q == 0)
-        return JANUS_OK;
-    hipStream_t st = as_stream(stream);
-    const int shift = __builtin_ctz((unsigned)page_size);
-    const float sl2 = scale * LOG2E;
-    const int of32 = out_dt == JANUS_F32;
-    if (splits == 1) {
-        launch_mla(bt, q, Hq, k_pool, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32, lse, 1,
-                   nullptr, st);
-        return launch_status();
-    }
-    float *part = static_cast<float *>(workspace);
-    launch_mla(bt, q, Hq, k_pool, k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32, lse, splits,
-               part, st);
-    if (hipGetLastError() != hipSuccess)
-        return JANUS_ERR_DEVICE;
-    hipLaunchKernelGGL(attn_combine, dim3((int64_t)bt->total_q * Hq), dim3(COMBINE_THREADS), 0, st, part, splits, Hq,
-                       MLA_DV, out, of32, lse);
-    return launch_status();
+    return run_mla<false>(bt, q, Hq, k_pool, 2 * k_row_stride, page_table, pt_ld, page_size, topk_idx, k, scale, out,
+                          out_dt, lse, num_splits, workspace, workspace_bytes, stream);
+}
+
+extern "C" int janus_sparse_attn_fp8kv(const janus_batch *bt, const void *q, int Hq, const uint8_t *kv_pool,
+                                       int64_t row_bytes, const int32_t *page_table, int pt_ld, int page_size,
+                                       const int32_t *topk_idx, int k, float scale, void *out, janus_dtype out_dt,
+                                       float *lse, int num_splits, void *workspace, size_t *workspace_bytes,
+                                       void *stream)
+{
+    if (!batch_ok(bt) || !q || !kv_pool || !page_table || !topk_idx || !out || !workspace_bytes || Hq < 1 ||
+        k < 1 || pt_ld < 1 || !pow2(page_size) || row_bytes < KV8_ROWB || num_splits < 0 ||
+        num_splits > MAX_SPLITS)
+        return JANUS_ERR_INVALID_ARG;
+    if (out_dt != JANUS_BF16 && out_dt != JANUS_F32)
+        return JANUS_ERR_UNSUPPORTED;
+    if ((row_bytes % 16) != 0 || (reinterpret_cast<uintptr_t>(kv_pool) & 15) != 0 ||
+        (reinterpret_cast<uintptr_t>(q) & 15) != 0 || k > MLA_MAX_K ||
+        !(Hq == 128 || Hq == 64 || Hq == 32 || Hq == 16))
+        return JANUS_ERR_UNSUPPORTED;
+    return run_mla<true>(bt, q, Hq, kv_pool, row_bytes, page_table, pt_ld, page_size, topk_idx, k, scale, out,
+                         out_dt, lse, num_splits, workspace, workspace_bytes, stream);
 }

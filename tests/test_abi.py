@@ -173,3 +173,21 @@ def test_entry_shift_out_of_range_is_rejected(L):
     b = _batch()
     b.entry_shift = 16
     assert L.janus_topk(ctypes.byref(b), FAKE, 7000, FAKE, None, ctypes.byref(ws), None) == 2  # accepted shift
+
+
+def test_fp8kv_attention_rejections(L):
+    b = _batch()
+    ws = ctypes.c_size_t(0)
+    call = lambda **kw: L.janus_sparse_attn_fp8kv(
+        ctypes.byref(b), kw.get("q", FAKE), kw.get("Hq", 128), kw.get("kv", FAKE), kw.get("rb", 592), FAKE, 4, 64,
+        FAKE, kw.get("k", 64), ctypes.c_float(0.1), FAKE, kw.get("odt", 1), None, kw.get("ns", 1), None,
+        ctypes.byref(ws), None)
+    assert call() == 0 and ws.value == 0  # size query: unsplit needs no workspace
+    assert call(rb=576) == 1              # row shorter than 576 bytes + scale
+    assert call(kv=None) == 1
+    assert call(ns=17) == 1
+    assert call(rb=600) == 2              # rows must be 16-byte multiples
+    assert call(Hq=48) == 2
+    assert call(k=5000) == 2
+    assert call(odt=2) == 2               # out dtype fp8
+    assert call(q=ctypes.c_void_p(0x1008)) == 2  # misaligned q

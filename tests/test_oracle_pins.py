@@ -635,3 +635,30 @@ def test_entry_attention_equals_token_attention_with_entry_masks(E):
     o2, l2 = oracle.sparse_attn([0, N], [C], rows, ai.q, *args, masked, ai.scale, ai.dv)
     assert np.array_equal(o1, o2) and np.array_equal(l1, l2)
     assert np.any(masked != sel)
+
+
+# ----------------------------------------------------------------------------- FP8 KV cache
+def test_fp8kv_attention_equals_bf16_attention_on_decoded_rows():
+    """With power-of-two row scales every stored value e4m3 * 2^e is a bf16
+    value, so attention over the fp8 rows equals the (separately pinned)
+    bf16 attention over the decoded rows bit for bit: the fp8 decode, the
+    scale's place in the row and V being the row's first 512 elements."""
+    from workloads import to_fp8_bytes
+    rng = np.random.default_rng(8)
+    M, N, ps, Hq = 60, 5, 8, 4
+    P = (M + N + ps - 1) // ps
+    x = rng.standard_normal((P * ps, 576)).astype(np.float32)
+    e = rng.integers(-12, 4, size=P * ps)
+    pool8 = np.zeros((P * ps, 592), np.uint8)
+    pool8[:, :576] = to_fp8_bytes(x * 16)
+    pool8[:, 576:580] = np.exp2(e).astype(np.float32).view(np.uint8).reshape(-1, 4)
+    dec = np.array([oracle.fp8_value(b) for b in range(256)])[pool8[:, :576]] * np.exp2(e)[:, None]
+    bf = to_bf16_bits(dec.astype(np.float32))
+    assert np.array_equal(np.array([oracle.bf16_value(b) for b in bf.reshape(-1)[:2000]]), dec.reshape(-1)[:2000])
+    pt = rng.permutation(P).astype(np.int32).reshape(1, P)
+    q = to_bf16_bits(rng.standard_normal((N, Hq, 576)).astype(np.float32))
+    sel = rng.integers(-1, M + N, size=(N, 16)).astype(np.int32)
+    rows = np.arange(N, dtype=np.int32)
+    o8, l8 = oracle.sparse_attn_fp8kv([0, N], [M], rows, q, pool8.reshape(P, ps, 592), pt, ps, sel, 0.05)
+    ob, lb = oracle.sparse_attn([0, N], [M], rows, q, bf, None, 576, 576, pt, ps, sel, 0.05, 512)
+    assert np.array_equal(o8, ob) and np.array_equal(l8, lb)

@@ -12,6 +12,8 @@ from .gen import (  # noqa: F401
     config,
     CONFIG_NAMES,
     attention_inputs,
+    attention_kv_fp8,
+    KV8_ROW_BYTES,
     attention_q_rows,
     to_fp8_bytes,
     to_bf16_bits,

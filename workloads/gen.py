@@ -422,6 +422,31 @@ def attention_inputs(wl: Workload, with_q: bool = True) -> AttnInputs:
     return AttnInputs(q=q, k_pool=k_pool, v_pool=v_pool, Hq=Hq, dqk=dqk, dv=dv, scale=float(a["scale"]))
 
 
+KV8_ROW_BYTES = 592  # 576 e4m3 bytes, the fp32 scale at byte 576, padding
+
+
+def attention_kv_fp8(wl: Workload) -> np.ndarray:
+    """The MLA KV pool of attention_inputs (the same draws) kept in fp8: uint8
+    [num_phys_pages, page_size, 592], each row 576 e4m3 bytes (amax/448 scale,
+    round-to-nearest-even cast) followed by its fp32 scale and zero padding."""
+    a = wl.attn_cfg
+    assert a["mla"] and a["dqk"] == 576
+    P, ps = wl.num_phys_pages, wl.page_size
+    pool = np.zeros((P, ps, KV8_ROW_BYTES), dtype=np.uint8)
+    kv_std = np.float32(a["kv_std"])
+    for b in range(wl.num_seqs):
+        npg = (int(wl.ctx_len[b]) + ps - 1) // ps
+        for lp in range(npg):
+            pp = int(wl.page_table[b, lp])
+            x = _rng(wl.seed, S_KV, wl.layer, b, lp, 0).standard_normal((ps, 576), dtype=np.float32)
+            if kv_std != 1.0:
+                x *= kv_std
+            q8, sc = quantize_fp8_per_row(x)
+            pool[pp, :, :576] = q8
+            pool[pp, :, 576:580] = sc.astype(np.float32).view(np.uint8).reshape(ps, 4)
+    return pool
+
+
 def synth_topk(wl: Workload, seed: int = 0, hot_frac: float = 0.6, pad_rows: int = 0) -> np.ndarray:
     """Selections shaped like real ones, without scoring anything.
 
