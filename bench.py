@@ -42,6 +42,9 @@ def parse():
     p.add_argument("--warmup", type=int, default=3)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the decode-phase measurement")
+    p.add_argument("--core-only", action="store_true",
+                   help="time the one-layer step only: no sharded sweep, decode, IndexShare or fp8-KV fields "
+                        "(for profiler passes)")
     p.add_argument("--cpu-rows", type=int, default=128, help="query rows in the oracle's timed sample")
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "index_scores_traffic.json"))
     p.add_argument("--copy-calibration", action="store_true",
@@ -156,12 +159,15 @@ def main():
 
     ms_step = wall / args.steps * 1e3
     counts = diff_out[2].cpu().tolist()
-    sharded = sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, pd_out[0], pt, ps, P, mr, k)
-    decode = decode_step(janus, torch, max(args.steps, 5)) if not args.no_decode else None
-    kv8 = fp8kv_attention(janus, torch, bt, qa, kv, pt, ps, sel, ai, max(args.steps, 5), per["sparse_attn"])
+    extras = not args.core_only
+    sharded = (sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, pd_out[0], pt, ps, P, mr, k)
+               if extras else None)
+    decode = decode_step(janus, torch, max(args.steps, 5)) if extras and not args.no_decode else None
+    kv8 = fp8kv_attention(janus, torch, bt, qa, kv, pt, ps, sel, ai, max(args.steps, 5), per["sparse_attn"]) \
+        if extras else None
     share = indexshare_group(janus, torch, step_calls=(bt, q, kI, w, sq, sk, pt, ps, P, mr, k, scores, sel, qa, kv,
                                                        pd_out, diff_out, pred_bm, out, lse, ai),
-                             steps=max(args.steps, 3))
+                             steps=max(args.steps, 3)) if extras else None
     rec = {
         "metric": "new tokens/s per layer (indexer+top-k+sparse attn) at 128K history; % MFMA/HBM peak",
         "value": N * args.steps / wall,
