@@ -38,7 +38,7 @@ namespace janus {
 
 constexpr int IDX_TPW = 2;                          // tokens per wave
 constexpr int IDX_WAVES = 4;                        // waves per block
-constexpr int IDX_KEY_CHUNK = 2048;                 // keys per block
+constexpr int IDX_KEY_CHUNK = 16384;                // target keys per block: long blocks spread each block's query and weight loads over more keys
 constexpr int GEN_TOK_TILE = 8;                     // vector kernel: tokens per block
 constexpr int GEN_KEY_TILE = 32;                    // vector kernel: keys per block
 
@@ -723,7 +723,7 @@ extern "C" int janus_index_scores(const janus_batch *bt, const void *q, janus_dt
     }
     if (q_dt == JANUS_FP8_E4M3 && d == 128 && H == 64 && bt->max_ctx <= (1 << 24)) {
         // key chunks: a multiple of the XCD count, each a whole number of
-        // stages and about IDX_KEY_CHUNK keys long
+        // stages and at most IDX_KEY_CHUNK keys long
         const int per_xcd_keys = ceil_div(bt->max_ctx, IDX_XCD);
         const int chunks_per_xcd = std::max(1, ceil_div(per_xcd_keys, IDX_KEY_CHUNK));
         const int key_chunk = ceil_div(ceil_div(per_xcd_keys, chunks_per_xcd), IDX_STAGE) * IDX_STAGE;
