@@ -30,7 +30,7 @@ def test_header_declares_the_five_calls():
     syms = declared_symbols()
     for s in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
               "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split", "janus_index_scores_mxfp4",
-              "janus_status_string"):
+              "janus_sparse_attn_fp8kv", "janus_status_string"):
         assert s in syms
 
 
