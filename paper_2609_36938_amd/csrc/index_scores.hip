@@ -33,6 +33,7 @@
 #include "janus_host.hpp"
 
 #include <algorithm>
+#include <cmath>
 
 namespace janus {
 
@@ -490,7 +491,7 @@ __global__ __launch_bounds__(256) void index_scores_vector(
 namespace janus {
 
 // Row-tile kernel: a block takes up to NQ tokens of one session and one
-// 4096-key chunk.  It serves decode-shaped batches (every session appends at
+// chunk of 1024, 2048 or 4096 keys (chosen per launch).  It serves decode-shaped batches (every session appends at
 // most NQ tokens, as in the decode phase: the scores are a GEMV over each
 // session's keys, bound by reading the keys once) and MXFP4 keys at any size.
 // The four waves take the chunk's 64-key groups in turn; a wave reads a
@@ -502,20 +503,21 @@ namespace janus {
 // Groups wholly past every token's causal limit skip the MFMAs (their stores
 // write -inf).
 constexpr int ROWS_NQ = 4;
-constexpr int ROWS_CHUNK = 4096;   // keys per block
+constexpr int ROWS_CHUNK_MAX = 4096;   // keys per block: 4096, 2048 or 1024
+constexpr int ROWS_CHUNK_MIN = 1024;
 
 template <int NQ, bool FP4>
 __global__ __launch_bounds__(256, 2) void index_scores_rows(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
     const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs, int es, int nchunks,
-    int one_tile, const uint8_t *__restrict__ q, const float *__restrict__ q_scale, const uint8_t *__restrict__ kI,
+    int chunk, int one_tile, const uint8_t *__restrict__ q, const float *__restrict__ q_scale, const uint8_t *__restrict__ kI,
     const uint8_t *__restrict__ k_bscale, const float *__restrict__ k_scale, const float *__restrict__ w,
     float *__restrict__ scores)
 {
     // block = (tile, chunk), chunk fastest; with one tile per session the
     // tile is the session
     const int tile = blockIdx.x / nchunks;
-    const int c0 = (blockIdx.x - tile * nchunks) * ROWS_CHUNK;
+    const int c0 = (blockIdx.x - tile * nchunks) * chunk;
     int b = tile, t0 = 0;
     if (!one_tile && !tile_slot(q_start, num_seqs, tile, NQ, b, t0))
         return;
@@ -571,7 +573,7 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
         make_buffer_rsrc((void *)(k_scale ? k_scale + kbase : nullptr), k_scale ? (uint32_t)(ctx - c0) << 2 : 0u);
     const __amdgpu_buffer_rsrc_t srs =
         make_buffer_rsrc(scores + score_start[b] + (int64_t)t0 * ctx, (uint32_t)(nv * ctx) << 2);
-    const int ngroups = (min(ROWS_CHUNK, ctx - c0) + 63) / 64;
+    const int ngroups = (min(chunk, ctx - c0) + 63) / 64;
     int lim[NQ];  // each token's last candidate (block-uniform)
 #pragma unroll
     for (int t = 0; t < NQ; ++t)
@@ -669,22 +671,52 @@ static int64_t rows_tiles(const janus_batch *bt, int nq)
 static int rows_nq(const janus_batch *bt) { return bt->max_q <= 1 ? 1 : bt->max_q <= 2 ? 2 : ROWS_NQ; }
 static bool rows_grid_ok(const janus_batch *bt)
 {
-    return rows_tiles(bt, rows_nq(bt)) * ceil_div(bt->max_ctx, ROWS_CHUNK) <= INT32_MAX;
+    return rows_tiles(bt, rows_nq(bt)) * ceil_div(bt->max_ctx, ROWS_CHUNK_MIN) <= INT32_MAX;
 }
 
-// 1-D grid of the row-tile kernel: (tile, 4096-key chunk), chunk fastest
+// Keys per block.  A ragged batch's blocks fill the GPU's resident block
+// slots in rounds, the last one part-empty, and few blocks leave CUs idle:
+// of 4096, 2048 and 1024 keys, take the chunk whose estimated block count
+// fills its rounds best (ties, within 5%, go to the longer chunk, which
+// loads its tokens' queries once for more keys).  A session of C keys makes
+// about C/chunk + 1/2 blocks per tile.
+template <typename Kern>
+static int rows_chunk(const janus_batch *bt, int64_t tiles, Kern kern)
+{
+    int dev = 0, cus = 0, per = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, kern, 256, 0) != hipSuccess || cus < 1 || per < 1)
+        return ROWS_CHUNK_MAX;
+    const double slots = (double)per * cus;
+    const double tiles_per_seq = (double)tiles / bt->num_seqs;
+    int best = ROWS_CHUNK_MAX;
+    double best_fill = -1.0;
+    for (int c = ROWS_CHUNK_MAX; c >= ROWS_CHUNK_MIN; c /= 2) {
+        const double blocks = tiles_per_seq * ((double)bt->total_ctx / c + 0.5 * bt->num_seqs);
+        const double fill = blocks / (std::ceil(blocks / slots) * slots);
+        if (fill > best_fill + 0.05) {
+            best_fill = fill;
+            best = c;
+        }
+    }
+    return best;
+}
+
+// 1-D grid of the row-tile kernel: (tile, key chunk), chunk fastest
 template <bool FP4>
 static void launch_rows(const janus_batch *bt, const void *q, const float *q_scale, const void *kI,
                         const uint8_t *k_bscale, const float *k_scale, const float *w, float *scores, hipStream_t st)
 {
     const int nq = rows_nq(bt);
-    const int nchunks = ceil_div(bt->max_ctx, ROWS_CHUNK);
     const int one_tile = bt->max_q <= nq;
-    const dim3 grid((unsigned)(rows_tiles(bt, nq) * nchunks));
+    const int64_t tiles = rows_tiles(bt, nq);
     auto go = [&](auto kern) {
-        hipLaunchKernelGGL(kern, grid, dim3(256), 0, st, bt->q_start, bt->ctx_start, bt->hist_len, bt->score_start,
-                           bt->num_seqs, bt->entry_shift, nchunks, one_tile, (const uint8_t *)q, q_scale, (const uint8_t *)kI,
-                           k_bscale, k_scale, w, scores);
+        const int chunk = rows_chunk(bt, tiles, kern);
+        const int nchunks = ceil_div(bt->max_ctx, chunk);
+        hipLaunchKernelGGL(kern, dim3((unsigned)(tiles * nchunks)), dim3(256), 0, st, bt->q_start, bt->ctx_start,
+                           bt->hist_len, bt->score_start, bt->num_seqs, bt->entry_shift, nchunks, chunk, one_tile,
+                           (const uint8_t *)q, q_scale, (const uint8_t *)kI, k_bscale, k_scale, w, scores);
     };
     if (nq == 1)
         go(index_scores_rows<1, FP4>);
