@@ -114,6 +114,25 @@ JANUS_DEV void tile_chunk(int qch, int &r, int &c)
     }
 }
 
+// The same for chunk 64*j + lane with j wave-uniform: the division by the
+// row pitch is done once per wave, leaving each lane an add and a compare.
+template <bool KV8>
+JANUS_DEV void tile_chunk_j(int j, int lane, int &r, int &c)
+{
+    if constexpr (KV8) {
+        tile_chunk<true>(64 * j + lane, r, c);
+    } else {
+        const int base = 64 * j;
+        const int r0 = base / MLA_PCH, rem = base - r0 * MLA_PCH;
+        const int t = rem + lane;  // < 2 * MLA_PCH
+        const bool wrap = t >= MLA_PCH;
+        r = r0 + (wrap ? 1 : 0);
+        c = wrap ? t - MLA_PCH : t;
+        if (c >= MLA_CPR)
+            c = 0;
+    }
+}
+
 // 8 fp8 e4m3 values -> 8 bf16 (exact: e4m3 values are bf16 values)
 JANUS_DEV v8bf fp8x8_to_bf16(v2i x)
 {
@@ -172,7 +191,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     const int lim = last_cand(hist_len[b], g - q_start[b], es);  // last causal id
     const int32_t *pt = page_table + (int64_t)b * pt_ld;
     const int psz_mask = (1 << page_shift) - 1;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int c16 = lane & 15, grp = lane >> 4;
     const int head0 = 16 * wave;
 
@@ -211,12 +230,12 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             const int j = wave + NW * i;
             const int qch = 64 * j + lane;
             int r, c;
-            tile_chunk<KV8>(qch, r, c);
+            tile_chunk_j<KV8>(j, lane, r, c);
             const int key = MLA_KT * t + r;
             int slot = (qch < TILE_CH && key < kl) ? sSlot[key] : -1;
             if (slot < 0)
                 slot = 0;  // padding rows read a real row; their logits are masked
-            const uint8_t *src = kv + (int64_t)slot * row_bytes + 16 * c;
+            const uint8_t *src = kv + (uint64_t)(uint32_t)slot * (uint32_t)row_bytes + 16 * c;
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
         }
     };
@@ -232,7 +251,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         for (int u = 0; u < NG; ++u) {
             const int qch = 64 * (wave + NW * (I0 + u)) + ln;
             int r, c;
-            tile_chunk<KV8>(qch, r, c);
+            tile_chunk_j<KV8>(wave + NW * (I0 + u), ln, r, c);
             const int key = MLA_KT * t + r;
             slot[u] = (qch < TILE_CH && key < kl) ? sSlot[key] : -1;
             cc[u] = c;
@@ -241,7 +260,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         for (int u = 0; u < NG; ++u) {
             const int j = wave + NW * (I0 + u);
             const int sl = slot[u] < 0 ? 0 : slot[u];  // padding rows read a real row; their logits are masked
-            const uint8_t *src = kv + (int64_t)sl * row_bytes + 16 * cc[u];
+            const uint8_t *src = kv + (uint64_t)(uint32_t)sl * (uint32_t)row_bytes + 16 * cc[u];
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
         }
     };
@@ -652,7 +671,7 @@ static bool mla_shape(const void *q, int Hq, int dqk, int dv, const void *k_pool
                       int64_t k_row_stride, int64_t v_row_stride, int k)
 {
     return dqk == MLA_DQK && dv == MLA_DV && v_pool == k_pool && v_row_stride == k_row_stride &&
-           (k_row_stride % 8) == 0 && (reinterpret_cast<uintptr_t>(k_pool) & 15) == 0 &&
+           (k_row_stride % 8) == 0 && k_row_stride <= (1 << 30) && (reinterpret_cast<uintptr_t>(k_pool) & 15) == 0 &&
            (reinterpret_cast<uintptr_t>(q) & 15) == 0 && k <= MLA_MAX_K &&
            (Hq == 128 || Hq == 64 || Hq == 32 || Hq == 16);
 }
@@ -816,7 +835,7 @@ extern "C" int janus_sparse_attn_fp8kv(const janus_batch *bt, const void *q, int
         return JANUS_ERR_INVALID_ARG;
     if (out_dt != JANUS_BF16 && out_dt != JANUS_F32)
         return JANUS_ERR_UNSUPPORTED;
-    if ((row_bytes % 16) != 0 || (reinterpret_cast<uintptr_t>(kv_pool) & 15) != 0 ||
+    if ((row_bytes % 16) != 0 || row_bytes > INT32_MAX || (reinterpret_cast<uintptr_t>(kv_pool) & 15) != 0 ||
         (reinterpret_cast<uintptr_t>(q) & 15) != 0 || k > MLA_MAX_K ||
         !(Hq == 128 || Hq == 64 || Hq == 32 || Hq == 16))
         return JANUS_ERR_UNSUPPORTED;
