@@ -260,7 +260,8 @@ int janus_predict_diff(const uint32_t *actual, const uint32_t *predicted,
  * A row with no valid id gets out = 0 and lse = -inf.  Softmax and
  * accumulation are fp32; products run on bf16 MFMA for Hq in {16, 32, 64,
  * 128}, dqk = 576, dv = 512, v_pool == k_pool, k <= 4096, a row stride that
- * is a multiple of 8 and 16-byte aligned q and pool; otherwise on a plain
+ * is a multiple of 8 and at most 2^30, and 16-byte aligned q and pool;
+ * otherwise on a plain
  * vector kernel (dqk <= 1024, dv <= 1024), else JANUS_ERR_UNSUPPORTED.
  */
 int janus_sparse_attn(const janus_batch *b,
@@ -314,14 +315,15 @@ int janus_sparse_attn_split(const janus_batch *b,
  * first 512 elements.  The row of id s is pool row
  * page_table[b, s/page_size]*page_size + s%page_size, at kv_pool + that * row_bytes.
  *   q        device [total_q, Hq, 576] bf16, 16-byte aligned; Hq in {16, 32, 64, 128}
- *   kv_pool  device, 16-byte aligned; row_bytes >= 592 and a multiple of 16
+ *   kv_pool  device, 16-byte aligned; row_bytes >= 592, a multiple of 16 and
+ *            below 2^31
  *   k        <= 4096
  *   out, lse, num_splits, workspace, workspace_bytes: as janus_sparse_attn_split
  *            (num_splits = 1 runs unsplit and needs no workspace)
  * The stored values are exact in bf16: products run on bf16 MFMA, softmax and
  * accumulation in fp32.  Each key's scale multiplies its logit and, before the
  * bf16 rounding of the probabilities, its probability.  Shapes outside the
- * above return JANUS_ERR_UNSUPPORTED (alignment, Hq, k) or
+ * above return JANUS_ERR_UNSUPPORTED (alignment, row_bytes, Hq, k) or
  * JANUS_ERR_INVALID_ARG (row_bytes < 592, NULL pointers).
  */
 int janus_sparse_attn_fp8kv(const janus_batch *b,
