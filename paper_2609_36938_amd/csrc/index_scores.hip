@@ -70,8 +70,11 @@ constexpr int IDX_MFMA_SCALES = 0x7f66;
 // pair into acc.  The MFMA results live in v[112:127], declared clobbered, so
 // the group is one block whose wait states are written out (the counts the
 // compiler itself emits for these pairs of instructions): two ahead of the
-// MFMAs (a VALU write of one of their sources), twelve after them (an 8-pass
-// MFMA result read by the VALU), at least one between a convert and the dot
+// MFMAs (a VALU write of one of their sources); twelve between an 8-pass MFMA
+// and the VALU that reads its result, where each later 8-pass MFMA counts as
+// four (so one wait state after the fourth MFMA covers every read below: the
+// second MFMA's first convert comes three instructions later, the fourth's
+// eleven); at least one between a convert and the dot
 // product that reads its pair (each dot reads a pair converted two
 // instructions earlier; consecutive dots accumulating into one register need
 // none), and three at the end, before any other instruction reads the dot
@@ -81,7 +84,7 @@ constexpr int IDX_MFMA_SCALES = 0x7f66;
 #define IDX_HEAD_GROUP(INIT)                                                                         \
     INIT "s_nop 1\n\t" IDX_MFMA("v[112:115]", "a0") IDX_MFMA("v[116:119]", "a1") IDX_MFMA("v[120:123]", "a2") \
         IDX_MFMA("v[124:127]", "a3")                                                                  \
-    "s_nop 11\n\t"                                                                                    \
+    "s_nop 0\n\t"                                                                                     \
     "v_cvt_pk_bf16_f32 v112, v112, v113 clamp\n\t"                                                    \
     "v_cvt_pk_bf16_f32 v114, v114, v115 clamp\n\t"                                                    \
     "v_dot2c_f32_bf16 %[acc], v112, %[w00]\n\t"                                                       \
@@ -138,7 +141,7 @@ JANUS_DEV void head_group(float &acc, const v8i &a0, const v8i &a1, const v8i &a
 #define F4_DOT(r, w) "v_dot2c_f32_bf16 %[acc], v" #r ", %[" w "]\n\t"
 #define IDX_HEAD_GROUP_F4(INIT)                                                                          \
     INIT "s_nop 1\n\t" IDX_MFMA_F4("v[112:115]", "a0") IDX_MFMA_F4("v[116:119]", "a1")                    \
-        IDX_MFMA_F4("v[120:123]", "a2") IDX_MFMA_F4("v[124:127]", "a3") "s_nop 11\n\t"                   \
+        IDX_MFMA_F4("v[120:123]", "a2") IDX_MFMA_F4("v[124:127]", "a3") "s_nop 0\n\t"                    \
         F4_CVT(112, 113)                                                                                   \
         F4_CVT(114, 115) F4_MAX(112)                                                                       \
         F4_CVT(116, 117) F4_MAX(114) F4_DOT(112, "w00")                                                    \
