@@ -95,32 +95,20 @@ constexpr int mla_ipw() { return ((mla_tile_ch<KV8>() + 63) / 64 + NW - 1) / NW;
 template <int NW, bool KV8>
 constexpr int mla_buf_bytes() { return NW * mla_ipw<NW, KV8>() * 64 * 16; }
 
-// Tile chunk qch -> key row r and chunk c of that row.  Chunks that are not
-// part of a row (row padding, the fp8 gap) load chunk 0 of key r: a dummy.
+// Tile chunk 64*j + lane (j wave-uniform) -> key row r and chunk c of that
+// row.  Chunks that are not part of a row (bf16 row padding, the fp8 gap)
+// load chunk 0 of key r: a dummy.  For bf16 rows the division by the row
+// pitch is done once per wave, leaving each lane an add and a compare.
 template <bool KV8>
-JANUS_DEV void tile_chunk(int qch, int &r, int &c)
+JANUS_DEV void tile_chunk_j(int j, int lane, int &r, int &c)
 {
     if constexpr (KV8) {
+        const int qch = 64 * j + lane;
         const bool hi = qch >= 16 * KV8_CPR;
         const int q2 = hi ? qch - 16 * KV8_CPR - KV8_GAP : qch;
         const int rr = q2 < 0 ? 0 : q2 / KV8_CPR;
         r = rr + (hi ? 16 : 0);
         c = q2 < 0 ? 0 : q2 - rr * KV8_CPR;
-    } else {
-        r = qch / MLA_PCH;
-        c = qch - r * MLA_PCH;
-        if (c >= MLA_CPR)
-            c = 0;
-    }
-}
-
-// The same for chunk 64*j + lane with j wave-uniform: the division by the
-// row pitch is done once per wave, leaving each lane an add and a compare.
-template <bool KV8>
-JANUS_DEV void tile_chunk_j(int j, int lane, int &r, int &c)
-{
-    if constexpr (KV8) {
-        tile_chunk<true>(64 * j + lane, r, c);
     } else {
         const int base = 64 * j;
         const int r0 = base / MLA_PCH, rem = base - r0 * MLA_PCH;
