@@ -170,3 +170,54 @@ def test_entry_attention(shape):
         assert err <= 2e-2 and err <= 2e-2 * np.abs(ref[j]).max(), (g, err)
     fin = np.isfinite(lref)
     assert np.allclose(gl[fin], lref[fin], atol=2e-3)
+
+
+def test_entry_vector_kernels_and_sharded_topk():
+    """The generic kernels at entry granularity (E = 8): fp32 indexer scores
+    (4 heads x 64), top-k and the sharded top-k on the GPU's own scores (exact
+    against the oracle's selection over the same fp32 rows), and MQA attention
+    with separate K and V pools; two sessions, one shorter than an entry."""
+    from workloads.gen import MQA0_ATTN
+    E = 8
+    wl = make_workload(hist_len=[1500, 5], new_len=[70, 30], H=4, d=64, idx_dtype="f32", k=32, seed=51,
+                       attn=MQA0_ATTN, entry_shift=3, table="permuted", page_size=16)
+    bt = janus.Batch(wl.hist_len, wl.new_len, entry_shift=3)
+    sc = janus.index_scores(bt, T(wl.q), T(wl.kI), T(wl.w))
+    sel = janus.topk(bt, sc, wl.k)
+    shd = janus.topk_sharded(bt, sc, wl.k, 4, wl.page_size)
+    ai = attention_inputs(wl)
+    out, lse = janus.sparse_attn(bt, T(ai.q), T(ai.k_pool), T(ai.v_pool), T(wl.page_table), wl.page_size, sel,
+                                 ai.scale, dv=ai.dv, out_dtype="f32", want_lse=True)
+    torch.cuda.synchronize()
+    rows = np.arange(wl.total_q, dtype=np.int32)
+    ref = oracle.index_scores(wl.q_start, wl.hist_len, wl.q, "f32", None, wl.kI, "f32", None, wl.w, rows,
+                              out_ld=wl.max_ctx, entry=E)
+    flat = sc.cpu().numpy()
+    got = np.full((wl.total_q, wl.max_ctx), -np.inf)
+    for b in range(wl.num_seqs):
+        C = int(wl.ctx_len[b])
+        for i in range(int(wl.new_len[b])):
+            st = int(wl.score_start[b]) + i * C
+            got[wl.q_start[b] + i, :C] = flat[st: st + C]
+    fin = np.isfinite(ref)
+    assert np.array_equal(fin, np.isfinite(got))
+    assert np.allclose(got[fin], ref[fin], rtol=1e-5, atol=1e-4)
+    # selections on the GPU's own fp32 scores are exact
+    g32 = got.astype(np.float32)
+    assert np.array_equal(np.sort(sel.cpu().numpy(), axis=1),
+                          np.sort(oracle.topk(wl.q_start, wl.hist_len, rows, g32, wl.k, entry=E), axis=1))
+    want = oracle.topk_sharded(wl.q_start, wl.hist_len, rows, g32, wl.k, 4, wl.page_size, entry=E)
+    gs = shd.cpu().numpy()
+    kg = wl.k // 4
+    for n in range(4):
+        assert np.array_equal(np.sort(gs[:, n * kg:(n + 1) * kg], axis=1), np.sort(want[:, n * kg:(n + 1) * kg], axis=1))
+    gsel = sel.cpu().numpy()
+    oref, lref = oracle.sparse_attn(wl.q_start, wl.hist_len, rows, attention_q_rows(wl, rows), ai.k_pool, ai.v_pool,
+                                    ai.k_row_stride, ai.v_row_stride, wl.page_table, wl.page_size, gsel, ai.scale,
+                                    ai.dv, entry=E)
+    o = out.cpu().numpy()
+    assert np.allclose(o, oref, atol=2e-3, rtol=1e-2)
+    l = lse.cpu().numpy()
+    assert np.array_equal(np.isneginf(l), np.isneginf(lref))
+    assert np.allclose(l[np.isfinite(lref)], lref[np.isfinite(lref)], atol=1e-3)
+    assert np.isneginf(lref).any()  # session 2's first tokens have no whole entry
