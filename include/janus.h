@@ -288,7 +288,8 @@ int janus_sparse_attn(const janus_batch *b,
  *                    query the size (written to *workspace_bytes, nothing
  *                    launched): total_q * splits * Hq * 514 * 4 bytes, or 0
  *                    when one slice results.  Too small: JANUS_ERR_WORKSPACE.
- * Only the MFMA shape of janus_sparse_attn is supported (else
+ * Only the MFMA shape of janus_sparse_attn is supported, and with more than
+ * one slice the workspace and out must be 16-byte aligned (else
  * JANUS_ERR_UNSUPPORTED).  Calls on one stream may share a workspace; calls
  * that overlap in time need their own.
  */

@@ -506,18 +506,21 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
 // Merge of a selection split into S slices (flash-decoding): per (token,
 // head), with slice maxima m_s and sums l_s, M = max m_s, w_s = 2^(m_s - M),
 // O = sum_s w_s O_s / sum_s w_s l_s and lse = (M + log2 sum_s w_s l_s) ln 2.
-// One block per (token, head); thread t handles dims t, t + 256, ...
-constexpr int COMBINE_THREADS = 256;
+// One wave per (token, head), four heads per block; lane l handles dims
+// 8l .. 8l+7 with 16-byte loads and stores (dv = 512).
+constexpr int COMBINE_HEADS = 4;
+constexpr int COMBINE_THREADS = 64 * COMBINE_HEADS;
 constexpr int MAX_SPLITS = 16;
 
 __global__ __launch_bounds__(COMBINE_THREADS) void attn_combine(const float *__restrict__ part, int splits, int Hq,
                                                                 int dv, void *__restrict__ out, int out_f32,
                                                                 float *__restrict__ lse)
 {
-    const int64_t row = blockIdx.x;  // token * Hq + head
+    const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int64_t row = (int64_t)blockIdx.x * COMBINE_HEADS + w;  // token * Hq + head
     const int64_t g = row / Hq, h = row % Hq;
-    const int64_t nblk = (int64_t)gridDim.x / Hq * splits;  // slices over all tokens
-    const float *ml = part + nblk * Hq * dv;
+    const int64_t ntok = (int64_t)gridDim.x * COMBINE_HEADS / Hq;
+    const float *ml = part + ntok * splits * Hq * dv;
     float ms[MAX_SPLITS], M = -INFINITY;
 #pragma unroll
     for (int sp = 0; sp < MAX_SPLITS; ++sp) {
@@ -532,19 +535,28 @@ __global__ __launch_bounds__(COMBINE_THREADS) void attn_combine(const float *__r
             L += ms[sp] * ml[((g * splits + sp) * Hq + h) * 2 + 1];
     }
     const float inv = L > 0.f ? 1.f / L : 0.f;
-    for (int d = threadIdx.x; d < dv; d += COMBINE_THREADS) {
-        float acc = 0.f;
+    v4f acc0 = v4f{0.f, 0.f, 0.f, 0.f}, acc1 = acc0;
 #pragma unroll
-        for (int sp = 0; sp < MAX_SPLITS; ++sp)
-            if (sp < splits)
-                acc = fmaf(ms[sp], part[((g * splits + sp) * Hq + h) * dv + d], acc);
-        const float v = acc * inv;
-        if (out_f32)
-            ((float *)out)[row * dv + d] = v;
-        else
-            ((uint16_t *)out)[row * dv + d] = f32_to_bf16_rne(v);
+    for (int sp = 0; sp < MAX_SPLITS; ++sp)
+        if (sp < splits) {
+            const v4f *src = (const v4f *)(part + ((g * splits + sp) * Hq + h) * dv) + 2 * lane;
+            acc0 += ms[sp] * src[0];
+            acc1 += ms[sp] * src[1];
+        }
+    acc0 *= inv;
+    acc1 *= inv;
+    if (out_f32) {
+        v4f *dst = (v4f *)((float *)out + row * dv) + 2 * lane;
+        dst[0] = acc0;
+        dst[1] = acc1;
+    } else {
+        const uint32_t p0 = f32_to_bf16_rne(acc0[0]) | ((uint32_t)f32_to_bf16_rne(acc0[1]) << 16);
+        const uint32_t p1 = f32_to_bf16_rne(acc0[2]) | ((uint32_t)f32_to_bf16_rne(acc0[3]) << 16);
+        const uint32_t p2 = f32_to_bf16_rne(acc1[0]) | ((uint32_t)f32_to_bf16_rne(acc1[1]) << 16);
+        const uint32_t p3 = f32_to_bf16_rne(acc1[2]) | ((uint32_t)f32_to_bf16_rne(acc1[3]) << 16);
+        ((v4i *)((uint16_t *)out + row * dv))[lane] = v4i{(int)p0, (int)p1, (int)p2, (int)p3};
     }
-    if (lse && threadIdx.x == 0)
+    if (lse && lane == 0)
         lse[row] = L > 0.f ? (M + log2f(L)) * LN2 : -INFINITY;
 }
 
@@ -729,6 +741,9 @@ static int run_mla(const janus_batch *bt, const void *q, int Hq, const void *poo
     }
     if (*workspace_bytes < need)
         return JANUS_ERR_WORKSPACE;
+    // the slice merge moves 16 bytes per lane
+    if (splits > 1 && (((reinterpret_cast<uintptr_t>(workspace) | reinterpret_cast<uintptr_t>(out)) & 15) != 0))
+        return JANUS_ERR_UNSUPPORTED;
     if (bt->total_q == 0)
         return JANUS_OK;
     hipStream_t st = as_stream(stream);
@@ -745,8 +760,9 @@ static int run_mla(const janus_batch *bt, const void *q, int Hq, const void *poo
                     part, st);
     if (hipGetLastError() != hipSuccess)
         return JANUS_ERR_DEVICE;
-    hipLaunchKernelGGL(attn_combine, dim3((int64_t)bt->total_q * Hq), dim3(COMBINE_THREADS), 0, st, part, splits, Hq,
-                       MLA_DV, out, of32, lse);
+    // Hq is a multiple of COMBINE_HEADS (16 .. 128) and dv = 512 = 64 lanes x 8
+    hipLaunchKernelGGL(attn_combine, dim3((int64_t)bt->total_q * Hq / COMBINE_HEADS), dim3(COMBINE_THREADS), 0, st,
+                       part, splits, Hq, MLA_DV, out, of32, lse);
     return launch_status();
 }
 

@@ -137,6 +137,11 @@ def test_split_attention_workspace_and_rejections(L):
     assert call(2, None, need, dqk=128, dv=128) == 2              # only the MFMA shape splits
     assert call(2, None, need, v=ctypes.c_void_p(0x2000)) == 2    # separate V pool
     assert call(2, None, need, odt=2) == 2                        # fp8 output
+    big = ctypes.c_size_t(1 << 40)
+    assert call(4, ctypes.c_void_p(0x1008), big) == 2             # slice merge needs a 16-byte aligned workspace
+    assert L.janus_sparse_attn_split(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 576, 576, FAKE, 4, 64, FAKE,
+                                     2048, f, ctypes.c_void_p(0x1004), 1, None, 4, FAKE, ctypes.byref(big),
+                                     None) == 2                  # ... and a 16-byte aligned output
 
 
 def test_product_path_does_not_touch_the_oracle():
