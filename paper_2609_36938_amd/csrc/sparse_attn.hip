@@ -252,36 +252,28 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
         }
     };
-    // the gathers of tile t+2 go out one at a time inside the S loop (with
-    // eight waves: at K-steps 0, 4, 8, 12 and 16), so that an issue stalled
-    // behind the gather queue overlaps MFMAs already in flight instead of
-    // holding every wave at the top of the step; other wave counts issue
-    // them all at step 0
-    constexpr bool SPREAD = IPW == 5 || (KV8 && IPW >= 2);
+    // the gathers of tile t+2 go out in five groups inside the S loop (at
+    // K-steps 0, 4, 8, 12 and 16; with eight waves one instruction each, with
+    // four two), so that an issue stalled behind the gather queue overlaps
+    // MFMAs already in flight instead of holding every wave at the top of
+    // the step; other wave counts issue them all at step 0
+    constexpr bool SPREAD = IPW == 5 || IPW == 10 || (KV8 && IPW >= 2);
+    auto spread_part = [&](auto Qc, int t, uint8_t *__restrict__ dst) {
+        constexpr int Q = decltype(Qc)::value;
+        constexpr int I0 = IPW <= 5 ? Q : Q * IPW / 5;
+        constexpr int I1 = IPW <= 5 ? (Q < IPW ? Q + 1 : Q) : (Q + 1) * IPW / 5;
+        if constexpr (I1 > I0)
+            issue_group(std::integral_constant<int, I0>{}, std::integral_constant<int, I1>{}, t, dst);
+    };
     auto issue_part = [&](int t, int part, uint8_t *__restrict__ dst) {
         if (t + 2 < ntiles) {
             if constexpr (SPREAD) {
                 switch (part) {
-                case 0:
-                    if constexpr (IPW > 0)
-                        issue_group(std::integral_constant<int, 0>{}, std::integral_constant<int, 1>{}, t + 2, dst);
-                    break;
-                case 1:
-                    if constexpr (IPW > 1)
-                        issue_group(std::integral_constant<int, 1>{}, std::integral_constant<int, 2>{}, t + 2, dst);
-                    break;
-                case 2:
-                    if constexpr (IPW > 2)
-                        issue_group(std::integral_constant<int, 2>{}, std::integral_constant<int, 3>{}, t + 2, dst);
-                    break;
-                case 3:
-                    if constexpr (IPW > 3)
-                        issue_group(std::integral_constant<int, 3>{}, std::integral_constant<int, 4>{}, t + 2, dst);
-                    break;
-                case 4:
-                    if constexpr (IPW > 4)
-                        issue_group(std::integral_constant<int, 4>{}, std::integral_constant<int, 5>{}, t + 2, dst);
-                    break;
+                case 0: spread_part(std::integral_constant<int, 0>{}, t + 2, dst); break;
+                case 1: spread_part(std::integral_constant<int, 1>{}, t + 2, dst); break;
+                case 2: spread_part(std::integral_constant<int, 2>{}, t + 2, dst); break;
+                case 3: spread_part(std::integral_constant<int, 3>{}, t + 2, dst); break;
+                case 4: spread_part(std::integral_constant<int, 4>{}, t + 2, dst); break;
                 default: break;
                 }
             } else if (part == 0) {
@@ -292,31 +284,36 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     auto tile_step = [&](int t, const uint8_t *__restrict__ tile, uint8_t *__restrict__ next) {
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
         v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
-        if constexpr (KV8) {
-            // fp8 rows: 8 bytes per lane and step, widened to bf16 in registers
-            const uint8_t *row0 = tile + kv8_key_off(c16) + 8 * grp;
-            const uint8_t *row1 = tile + kv8_key_off(c16 + 16) + 8 * grp;
+        // K operands: 16 bytes (bf16) or 8 bytes (fp8, widened to bf16 in
+        // registers) per lane and K-step for keys c16 and c16 + 16.  Q and O
+        // fill most of the registers, so the compiler alone keeps too few
+        // operand reads in flight: each step loads the next step's operands
+        // into a two-entry ring, and a scheduling fence per step keeps it
+        // from hoisting more than that
+        using KRaw = std::conditional_t<KV8, v2i, v4i>;
+        constexpr int SB = KV8 ? 32 : 64;  // bytes per K-step
+        const uint8_t *row0 = KV8 ? tile + kv8_key_off(c16) + 8 * grp : tile + c16 * MLA_ROWB + 16 * grp;
+        const uint8_t *row1 = KV8 ? tile + kv8_key_off(c16 + 16) + 8 * grp : row0 + 16 * MLA_ROWB;
+        auto widen = [](KRaw x) {
+            if constexpr (KV8)
+                return fp8x8_to_bf16(x);
+            else
+                return as_v8bf(x);
+        };
+        KRaw ring[2][2];
+        ring[0][0] = *(const KRaw *)row0;
+        ring[0][1] = *(const KRaw *)row1;
 #pragma unroll
-            for (int step = 0; step < MLA_STEPS; ++step) {
-                const v2i a0 = *(const v2i *)(row0 + 32 * step);
-                const v2i a1 = *(const v2i *)(row1 + 32 * step);
-                st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(a0), qf[step], st0, 0, 0, 0);
-                st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(a1), qf[step], st1, 0, 0, 0);
-                if (step % 4 == 0)
-                    issue_part(t, step / 4, next);
+        for (int step = 0; step < MLA_STEPS; ++step) {
+            if (step + 1 < MLA_STEPS) {
+                ring[(step + 1) & 1][0] = *(const KRaw *)(row0 + SB * (step + 1));
+                ring[(step + 1) & 1][1] = *(const KRaw *)(row1 + SB * (step + 1));
             }
-        } else {
-            const uint8_t *row0 = tile + c16 * MLA_ROWB + 16 * grp;
-            const uint8_t *row1 = row0 + 16 * MLA_ROWB;
-#pragma unroll
-            for (int step = 0; step < MLA_STEPS; ++step) {
-                const v4i a0 = *(const v4i *)(row0 + 64 * step);
-                const v4i a1 = *(const v4i *)(row1 + 64 * step);
-                st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a0), qf[step], st0, 0, 0, 0);
-                st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(a1), qf[step], st1, 0, 0, 0);
-                if (step % 4 == 0)
-                    issue_part(t, step / 4, next);
-            }
+            st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step & 1][0]), qf[step], st0, 0, 0, 0);
+            st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step & 1][1]), qf[step], st1, 0, 0, 0);
+            if (step % 4 == 0)
+                issue_part(t, step / 4, next);
+            __builtin_amdgcn_sched_barrier(0);
         }
         // online softmax (exp2 domain) with lazy rescaling of O.  Valid keys
         // of the tile come as a 32-bit mask (lanes 32-63 repeat 0-31); this
@@ -405,9 +402,19 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                 bv[nl] = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
             }
         }
+        // head blocks rescaled this tile, read together (wave-uniform)
+        uint32_t rmask = 0;
+#pragma unroll
+        for (int hb = 0; hb < NW; ++hb)
+            rmask |= (sResc[hb] != 0 ? 1u : 0u) << hb;
+        // P fragments one head block ahead
+        v4i pf[2];
+        pf[0] = sP[lane];
 #pragma unroll
         for (int hb = 0; hb < NW; ++hb) {
-            if (sResc[hb]) {  // wave-uniform
+            if (hb + 1 < NW)
+                pf[(hb + 1) & 1] = sP[64 * (hb + 1) + lane];
+            if (rmask & (1u << hb)) {
                 float ai[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
@@ -418,7 +425,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                     for (int i = 0; i < 4; ++i)
                         o[hb][nl][i] *= ai[i];
             }
-            const v8bf ph = __builtin_bit_cast(v8bf, sP[64 * hb + lane]);
+            const v8bf ph = __builtin_bit_cast(v8bf, pf[hb & 1]);
 #pragma unroll
             for (int nl = 0; nl < NBW; ++nl)
                 o[hb][nl] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, bv[nl], o[hb][nl], 0, 0, 0);
