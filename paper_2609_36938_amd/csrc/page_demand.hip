@@ -7,12 +7,15 @@
 // id to its physical page and sets it in an LDS bitmap (read-before-set, so
 // the hot pages that every row selects cost one LDS read, not an atomic);
 // the block then ORs its non-empty words into the global bitmap.
-// Runs and lists: one 1024-thread block walks the bitmap; each thread owns a
+// Runs and lists: one 1024-thread block stages the bitmap in LDS (at most
+// 64 KB) and walks it there; each thread owns a
 // contiguous word range, and block-wide scans give it the page-list offset,
 // the run offset, the last unset page before its range (where the run it
 // starts in began) and the first unset page after it (where a run ends).
 #include "janus_device.hpp"
 #include "janus_host.hpp"
+
+#include <algorithm>
 
 namespace janus {
 
@@ -157,8 +160,10 @@ JANUS_DEV void emit_list_runs(RunShared &sh, Words words, int nbits, int max_run
     // first walk: count run starts
     auto walk = [&](bool emit, int run_pos) -> int {
         int nstart = 0;
-        int lz = lz_before;      // last unset page seen so far
         int prev = (w0 << 5) - 1;
+        // (p - start of p's run) mod max_run, carried from page to page; the
+        // first page of this range may continue a run that began before it
+        int rem = -1;
         int pos = page_off;
         for (int w = w0; w < w1; ++w) {
             uint32_t v = word(w);
@@ -166,11 +171,15 @@ JANUS_DEV void emit_list_runs(RunShared &sh, Words words, int nbits, int max_run
                 const int p = (w << 5) + __ffs(v) - 1;
                 v &= v - 1u;
                 if (p != prev + 1)
-                    lz = p - 1;
+                    rem = 0;
+                else if (rem < 0)
+                    rem = (p - (lz_before + 1)) % max_run;
+                else
+                    rem = rem + 1 == max_run ? 0 : rem + 1;
                 prev = p;
                 if (emit && list)
                     list[pos++] = p;
-                if (((p - (lz + 1)) % max_run) == 0) {
+                if (rem == 0) {
                     if (emit) {
                         // run ends at the first unset page after p
                         int ez = end_zero;
@@ -210,7 +219,12 @@ __global__ __launch_bounds__(RUN_THREADS) void page_list_runs(const uint32_t *__
                                                               int32_t *__restrict__ runs, int32_t *__restrict__ counts)
 {
     __shared__ RunShared sh;
-    emit_list_runs(sh, [&](int w) { return bitmap[w]; }, nbits, max_run, list, runs, counts, counts + 1);
+    extern __shared__ uint32_t sw[];  // the bitmap's words
+    const int nwords = (nbits + 31) >> 5;
+    for (int w = threadIdx.x; w < nwords; w += RUN_THREADS)
+        sw[w] = bitmap[w];
+    __syncthreads();
+    emit_list_runs(sh, [&](int w) { return sw[w]; }, nbits, max_run, list, runs, counts, counts + 1);
 }
 
 __global__ __launch_bounds__(RUN_THREADS) void predict_diff_kernel(
@@ -219,6 +233,7 @@ __global__ __launch_bounds__(RUN_THREADS) void predict_diff_kernel(
 {
     __shared__ RunShared sh;
     __shared__ int32_t red[3][RUN_WAVES];
+    extern __shared__ uint32_t sw[];  // the miss set's words
     const int nwords = (nbits + 31) >> 5;
     int ca = 0, cp = 0, cap = 0;
     for (int w = threadIdx.x; w < nwords; w += RUN_THREADS) {
@@ -232,6 +247,7 @@ __global__ __launch_bounds__(RUN_THREADS) void predict_diff_kernel(
         cp += __popc(p);
         cap += __popc(a & p);
         miss[w] = a & ~p;
+        sw[w] = a & ~p;
     }
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
@@ -245,7 +261,7 @@ __global__ __launch_bounds__(RUN_THREADS) void predict_diff_kernel(
         red[1][wave] = cp;
         red[2][wave] = cap;
     }
-    __syncthreads();  // also orders the miss writes before the run walk reads them
+    __syncthreads();  // also orders the staged miss words before the run walk reads them
     if (threadIdx.x == 0) {
         int a = 0, p = 0, ap = 0;
         for (int w = 0; w < RUN_WAVES; ++w) {
@@ -258,8 +274,7 @@ __global__ __launch_bounds__(RUN_THREADS) void predict_diff_kernel(
         counts[2] = ap;
         counts[3] = a - ap;
     }
-    emit_list_runs(sh, [&](int w) { return actual[w] & ~predicted[w]; }, nbits, max_run, nullptr, miss_runs,
-                   nullptr, counts + 4);
+    emit_list_runs(sh, [&](int w) { return sw[w]; }, nbits, max_run, nullptr, miss_runs, nullptr, counts + 4);
 }
 
 } // namespace janus
@@ -294,8 +309,8 @@ extern "C" int janus_page_demand(const janus_batch *bt, const int32_t *topk_idx,
                            shift, limit,
                            nwords, bitmap);
     }
-    hipLaunchKernelGGL(page_list_runs, dim3(1), dim3(RUN_THREADS), 0, st, bitmap, num_phys_pages, max_run,
-                       page_list, runs, counts);
+    hipLaunchKernelGGL(page_list_runs, dim3(1), dim3(RUN_THREADS), std::max(nwords, 1) * sizeof(uint32_t), st, bitmap,
+                       num_phys_pages, max_run, page_list, runs, counts);
     return launch_status();
 }
 
@@ -306,7 +321,8 @@ extern "C" int janus_predict_diff(const uint32_t *actual, const uint32_t *predic
         return JANUS_ERR_INVALID_ARG;
     if (num_phys_pages > PD_MAX_PAGES)
         return JANUS_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL(predict_diff_kernel, dim3(1), dim3(RUN_THREADS), 0, as_stream(stream), actual, predicted,
-                       num_phys_pages, max_run, miss, miss_runs, counts);
+    const int nwords = (num_phys_pages + 31) >> 5;
+    hipLaunchKernelGGL(predict_diff_kernel, dim3(1), dim3(RUN_THREADS), std::max(nwords, 1) * sizeof(uint32_t),
+                       as_stream(stream), actual, predicted, num_phys_pages, max_run, miss, miss_runs, counts);
     return launch_status();
 }

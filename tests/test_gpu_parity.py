@@ -192,6 +192,31 @@ def test_page_demand_bit_exact(table, page_size, max_run):
         assert np.array_equal(runs.cpu().numpy()[: 2 * c[1]].reshape(-1, 2), rruns)
 
 
+def test_page_demand_largest_pool():
+    """The largest pool the call takes (2^19 pages: a 64 KB bitmap, staged
+    whole in LDS by the run walk), with the selection's pages spread over it
+    by a sparse page table; bit-exact against the oracle."""
+    P = 1 << 19
+    wl = make_workload(hist_len=[30000, 777], new_len=[40, 9], H=2, d=8, idx_dtype="f32", k=512, seed=4)
+    rng = np.random.default_rng(12)
+    table = rng.choice(P - 16, size=wl.page_table.size, replace=False).astype(np.int32)
+    table = table.reshape(wl.page_table.shape)
+    # the short session (786 tokens in 13 pages, 512 of them selected per
+    # row) sits on the pool's last pages: a run that ends at the pool's end
+    table[1, :13] = np.arange(P - 13, P, dtype=np.int32)
+    sel = synth_topk(wl, seed=5)
+    bt = _batch(wl)
+    bm, lst, runs, cnt = janus.page_demand(bt, T(sel), T(table), wl.page_size, P, 32)
+    torch.cuda.synchronize()
+    rbm, rlst, rc = oracle.page_demand(wl.q_start, wl.hist_len, sel, table, wl.page_size, P)
+    rruns = oracle.runs(rbm, P, 32)
+    c = cnt.cpu().numpy()
+    assert c[0] == rc and c[1] == rruns.shape[0]
+    assert np.array_equal(bm.cpu().numpy().view(np.uint32), rbm)
+    assert np.array_equal(lst.cpu().numpy()[:rc], rlst)
+    assert np.array_equal(runs.cpu().numpy()[: 2 * c[1]].reshape(-1, 2), rruns)
+
+
 def test_page_demand_edges():
     wl = make_workload(hist_len=[4096], new_len=[8], H=2, d=8, idx_dtype="f32", k=64, seed=1)
     bt = _batch(wl)
@@ -210,7 +235,7 @@ def test_page_demand_edges():
 
 def test_predict_diff_bit_exact():
     rng = np.random.default_rng(9)
-    for P, max_run in [(2176, 32), (7557, 32), (100, 1), (33, 4), (1, 32)]:
+    for P, max_run in [(2176, 32), (7557, 32), (100, 1), (33, 4), (1, 32), (1 << 19, 32)]:
         nw = (P + 31) // 32
         for dens in (0.05, 0.5, 0.97):
             A = (rng.random(nw * 32) < dens).reshape(nw, 32)
