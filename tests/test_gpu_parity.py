@@ -53,7 +53,9 @@ def _score_check(wl, got_rows, tol):
     fin = np.isfinite(ref)
     assert np.array_equal(fin, np.isfinite(got_rows)), "causal -inf pattern differs"
     assert np.all(np.isneginf(got_rows[~fin]))
-    err = np.where(fin, np.abs(got_rows.astype(np.float64) - ref), 0.0).max(axis=1)
+    diff = np.zeros(ref.shape)
+    diff[fin] = np.abs(got_rows[fin].astype(np.float64) - ref[fin])  # masked cells are -inf on both sides
+    err = diff.max(axis=1)
     scale = np.where(fin, np.abs(ref), 0.0).max(axis=1)
     rel = err / np.maximum(scale, 1e-300)
     assert rel.max() <= tol, f"row rel err {rel.max():.3e} > {tol}"
