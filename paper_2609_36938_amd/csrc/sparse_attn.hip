@@ -11,8 +11,9 @@
 //     are never drained early.
 //   * Wave w holds the queries of heads 16w..16w+15 in registers and forms
 //     S^T = K Q^T for them from the row-major tile (one 16-byte read per
-//     lane), so that each lane's outputs are 8 keys of one head: exactly an
-//     A operand of the P V product.  Softmax is online in the exp2 domain;
+//     lane, loaded one K-step ahead), so that each lane's outputs are 8 keys
+//     of one head: exactly an A operand of the P V product.  Softmax is
+//     online in the exp2 domain;
 //     the running max moves only when a logit exceeds it by a slack, and the
 //     cross-lane max reduction runs only then.
 //   * The waves exchange their P fragments (1 KB each) and rescale factors
