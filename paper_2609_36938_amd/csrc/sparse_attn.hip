@@ -301,6 +301,11 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             else
                 return as_v8bf(x);
         };
+        // fp8 rows: the waves raise their priority over the MFMA loops, so
+        // that a wave still in them is issued ahead of one in the widening
+        // or softmax VALU work (measured 3% faster; no gain with bf16 rows)
+        if constexpr (KV8)
+            __builtin_amdgcn_s_setprio(1);
         KRaw ring[2][2];
         ring[0][0] = *(const KRaw *)row0;
         ring[0][1] = *(const KRaw *)row1;
@@ -316,6 +321,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                 issue_part(t, step / 4, next);
             __builtin_amdgcn_sched_barrier(0);
         }
+        if constexpr (KV8)
+            __builtin_amdgcn_s_setprio(0);
         // online softmax (exp2 domain) with lazy rescaling of O.  Valid keys
         // of the tile come as a 32-bit mask (lanes 32-63 repeat 0-31); this
         // lane's keys are 16*kb + 4*grp + i
@@ -403,6 +410,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                 bv[nl] = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
             }
         }
+        if constexpr (KV8)
+            __builtin_amdgcn_s_setprio(1);
         // head blocks rescaled this tile, read together (wave-uniform)
         uint32_t rmask = 0;
 #pragma unroll
@@ -431,6 +440,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             for (int nl = 0; nl < NBW; ++nl)
                 o[hb][nl] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ph, bv[nl], o[hb][nl], 0, 0, 0);
         }
+        if constexpr (KV8)
+            __builtin_amdgcn_s_setprio(0);
         // tile t+1 has landed once at most tile t+2's gathers are pending; the
         // barrier also frees this tile's buffer for the gather of tile t+3
         if (t + 2 < ntiles)
