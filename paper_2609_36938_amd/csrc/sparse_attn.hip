@@ -13,9 +13,8 @@
 //     S^T = K Q^T for them from the row-major tile (one 16-byte read per
 //     lane, loaded one K-step ahead), so that each lane's outputs are 8 keys
 //     of one head: exactly an A operand of the P V product.  Softmax is
-//     online in the exp2 domain;
-//     the running max moves only when a logit exceeds it by a slack, and the
-//     cross-lane max reduction runs only then.
+//     online in the exp2 domain; the running max moves only when a logit
+//     exceeds it by a slack, and the cross-lane max reduction runs only then.
 //   * The waves exchange their P fragments (1 KB each) and rescale factors
 //     through LDS, and wave w then computes O for all heads over its own
 //     slice of 512/NW output dims, reading V through the transposing LDS
