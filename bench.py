@@ -319,7 +319,7 @@ def fp8kv_attention(janus, torch, bt, qa, kv, pt, ps, sel, ai, steps, bf16_ms):
 
 
 def indexshare_group(janus, torch, step_calls, steps):
-    """IndexShare (GLM-5 series, Sec. 2.1): four consecutive sparse-attention
+    """IndexShare (GLM-5 series, Sec. 2.2): four consecutive sparse-attention
     layers share one selection, and only the first runs the indexer and top-k.
     One group at the 128K workload: scores -> top-k -> page demand ->
     corrective set (once: the four layers' KV pools share the page table, so

@@ -35,13 +35,17 @@
  *     caller's next synchronisation.
  *   - Workspace: when a call takes (workspace, workspace_bytes), passing
  *     workspace == NULL stores the required byte count in *workspace_bytes and
- *     returns JANUS_OK without enqueuing anything.  The workspace needs no
+ *     returns JANUS_OK without enqueuing anything, also when that count is 0:
+ *     to run, pass a non-NULL workspace (any pointer when 0 bytes are needed;
+ *     it is then never dereferenced).  The workspace needs no
  *     initialisation.  Calls that share a workspace must not overlap.
  *   - Token ids are session-local: ids 0..M_b-1 are the cached history and
  *     M_b..M_b+N_b-1 the appended tokens.  In id arrays, values outside
  *     [0, M_b+N_b) are padding, like -1.
  *   - Page tables map a session's logical page (id / page_size) to a physical
- *     page of one shared pool; entries must lie in [0, num_phys_pages).
+ *     page of one shared pool; entries must lie in [0, num_phys_pages).  A
+ *     table [B, pt_ld] must cover the longest session: pt_ld * page_size >=
+ *     max_ctx, else JANUS_ERR_INVALID_ARG (every call that takes one).
  *   - The library is stateless and reentrant.
  */
 #ifndef JANUS_H
@@ -74,7 +78,7 @@ typedef enum {
  * the paper's notation table).  Host fields size grids; device arrays locate
  * rows.  All device arrays are int32 except score_start.
  *
- * Entry granularity (the selection unit of DeepSeek-V4, Sec. 2.1 footnote;
+ * Entry granularity (the selection unit of DeepSeek-V4, Sec. 2.2 footnote;
  * the notation table applies to entries unchanged).  With entry_shift = e > 0
  * every candidate is an entry: one cached row (indexer key, KV) standing for
  * the E = 2^e consecutive tokens [E*j, E*j + E - 1], which exists once its
@@ -203,7 +207,7 @@ int janus_topk_sharded(const janus_batch *b, const float *scores, int k,
  *                                        0 <= s < min(limit_b, M_b+N_b) }
  *
  *   topk_idx   device [total_q, k] int32 session-local ids (others: padding)
- *   page_table device [B, pt_ld] int32
+ *   page_table device [B, pt_ld] int32, pt_ld * page_size >= max_ctx
  *   page_size  power of two >= 1
  *   limit      device [B] int32, or NULL for M_b (history pages only: the
  *              appended tokens' KV is produced in HBM and never loaded)
@@ -251,7 +255,8 @@ int janus_predict_diff(const uint32_t *actual, const uint32_t *predicted,
  * S_i = the ids of row i of topk_idx that lie in [0, M_b+i] (others are
  * padding).  K_s is the first dqk elements of pool row
  * (page_table[b, s/page_size]*page_size + s%page_size) of k_pool, V_s the
- * first dv elements of the same row of v_pool.
+ * first dv elements of the same row of v_pool.  page_table is [B, pt_ld]
+ * with pt_ld * page_size >= max_ctx.
  *   q       device [total_q, Hq, dqk] bf16
  *   k_pool  device bf16 rows of k_row_stride elements (>= dqk)
  *   v_pool  device bf16 rows of v_row_stride elements (>= dv); may equal k_pool
@@ -287,7 +292,8 @@ int janus_sparse_attn(const janus_batch *b,
  *   workspace        device scratch of *workspace_bytes bytes, or NULL to
  *                    query the size (written to *workspace_bytes, nothing
  *                    launched): total_q * splits * Hq * 514 * 4 bytes, or 0
- *                    when one slice results.  Too small: JANUS_ERR_WORKSPACE.
+ *                    when one slice results (then pass any non-NULL pointer
+ *                    to run).  Too small: JANUS_ERR_WORKSPACE.
  * Only the MFMA shape of janus_sparse_attn is supported, and with more than
  * one slice the workspace and out must be 16-byte aligned (else
  * JANUS_ERR_UNSUPPORTED).  Calls on one stream may share a workspace; calls
@@ -320,7 +326,9 @@ int janus_sparse_attn_split(const janus_batch *b,
  *            below 2^31
  *   k        <= 4096
  *   out, lse, num_splits, workspace, workspace_bytes: as janus_sparse_attn_split
- *            (num_splits = 1 runs unsplit and needs no workspace)
+ *            (num_splits = 1 runs unsplit and needs 0 bytes of workspace, but
+ *            workspace == NULL is still a size query that launches nothing:
+ *            pass any non-NULL pointer to run)
  * The stored values are exact in bf16: products run on bf16 MFMA, softmax and
  * accumulation in fp32.  Each key's scale multiplies its logit and, before the
  * bf16 rounding of the probabilities, its probability.  Shapes outside the

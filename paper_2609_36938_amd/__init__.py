@@ -106,6 +106,14 @@ def _dtype_code(t: torch.Tensor, dt: Optional[str]) -> int:
     raise JanusError(f"unsupported dtype {t.dtype}")
 
 
+def _table(batch: "Batch", page_table, page_size: int) -> int:
+    """pt_ld of a [B, pt_ld] page table, which must cover the longest session."""
+    pt_ld = int(page_table.shape[1])
+    if pt_ld * int(page_size) < batch.max_ctx:
+        raise JanusError(f"page table covers {pt_ld} x {page_size} ids, the longest session has {batch.max_ctx}")
+    return pt_ld
+
+
 class Batch:
     """A ragged batch of sessions: history lengths M_b and appended lengths N_b
     (tokens).  entry_shift = e > 0 selects entry granularity: candidates are
@@ -202,7 +210,7 @@ def page_demand(batch: Batch, topk_idx, page_table, page_size: int, num_phys_pag
     bm, lst, runs, counts = out
     ws = ctypes.c_size_t(0)
     rc = lib().janus_page_demand(batch.ref, _ptr(topk_idx), int(topk_idx.shape[1]), _ptr(page_table),
-                                 int(page_table.shape[1]), int(page_size), _ptr(limit), int(num_phys_pages),
+                                 _table(batch, page_table, page_size), int(page_size), _ptr(limit), int(num_phys_pages),
                                  int(max_run), _ptr(bm), _ptr(lst), _ptr(runs), _ptr(counts), None,
                                  ctypes.byref(ws), _stream(stream))
     _check(rc, "janus_page_demand")
@@ -242,7 +250,7 @@ def sparse_attn(batch: Batch, q, k_pool, v_pool, page_table, page_size: int, top
     if want_lse and lse is None:
         lse = torch.empty((batch.total_q, Hq), dtype=torch.float32, device=q.device)
     rc = lib().janus_sparse_attn(batch.ref, _ptr(q), Hq, dqk, dv, _ptr(k_pool), _ptr(v_pool), krs, vrs,
-                                 _ptr(page_table), int(page_table.shape[1]), int(page_size), _ptr(topk_idx),
+                                 _ptr(page_table), _table(batch, page_table, page_size), int(page_size), _ptr(topk_idx),
                                  int(topk_idx.shape[1]), float(scale), _ptr(out), odt[0], _ptr(lse),
                                  _stream(stream))
     _check(rc, "janus_sparse_attn")
@@ -255,8 +263,9 @@ def sparse_attn_split(batch: Batch, q, k_pool, v_pool, page_table, page_size: in
                       lse=None, workspace=None, stream=None):
     """janus_sparse_attn_split: as sparse_attn, each row's selection split
     over num_splits blocks (0: the library picks); returns (out, lse or None).
-    workspace: a device uint8 tensor of at least sparse_attn_split_workspace()
-    bytes, or None to allocate one here."""
+    workspace: a device uint8 tensor of at least the byte count the library
+    reports for these arguments (its NULL-workspace size query, made here
+    first), or None to allocate one here."""
     Hq, dqk = int(q.shape[-2]), int(q.shape[-1])
     krs = int(k_row_stride if k_row_stride is not None else k_pool.shape[-1])
     vrs = int(v_row_stride if v_row_stride is not None else v_pool.shape[-1])
@@ -267,8 +276,8 @@ def sparse_attn_split(batch: Batch, q, k_pool, v_pool, page_table, page_size: in
     if want_lse and lse is None:
         lse = torch.empty((batch.total_q, Hq), dtype=torch.float32, device=q.device)
     args = (batch.ref, _ptr(q), Hq, dqk, dv, _ptr(k_pool), _ptr(v_pool), krs, vrs, _ptr(page_table),
-            int(page_table.shape[1]), int(page_size), _ptr(topk_idx), int(topk_idx.shape[1]), float(scale), _ptr(out),
-            odt[0], _ptr(lse), int(num_splits))
+            _table(batch, page_table, page_size), int(page_size), _ptr(topk_idx), int(topk_idx.shape[1]),
+            float(scale), _ptr(out), odt[0], _ptr(lse), int(num_splits))
     need = ctypes.c_size_t(0)
     _check(lib().janus_sparse_attn_split(*args, None, ctypes.byref(need), _stream(stream)), "janus_sparse_attn_split")
     if workspace is None:
@@ -292,9 +301,9 @@ def sparse_attn_fp8kv(batch: Batch, q, kv_pool, page_table, page_size: int, topk
         out = torch.empty((batch.total_q, Hq, 512), dtype=odt[1], device=q.device)
     if want_lse and lse is None:
         lse = torch.empty((batch.total_q, Hq), dtype=torch.float32, device=q.device)
-    args = (batch.ref, _ptr(q), Hq, _ptr(kv_pool), row_bytes, _ptr(page_table), int(page_table.shape[1]),
-            int(page_size), _ptr(topk_idx), int(topk_idx.shape[1]), float(scale), _ptr(out), odt[0], _ptr(lse),
-            int(num_splits))
+    args = (batch.ref, _ptr(q), Hq, _ptr(kv_pool), row_bytes, _ptr(page_table),
+            _table(batch, page_table, page_size), int(page_size), _ptr(topk_idx), int(topk_idx.shape[1]),
+            float(scale), _ptr(out), odt[0], _ptr(lse), int(num_splits))
     need = ctypes.c_size_t(0)
     _check(lib().janus_sparse_attn_fp8kv(*args, None, ctypes.byref(need), _stream(stream)), "janus_sparse_attn_fp8kv")
     if workspace is None:

@@ -29,6 +29,13 @@ inline bool dtype_ok(int dt) { return dt == JANUS_F32 || dt == JANUS_BF16 || dt 
 
 inline bool pow2(int x) { return x > 0 && (x & (x - 1)) == 0; }
 
+// A page table of pt_ld entries per session covers every id of the longest
+// session (ids are read through it up to max_ctx - 1).  page_size > 0.
+inline bool table_covers(const janus_batch *b, int pt_ld, int page_size)
+{
+    return pt_ld >= 1 && (int64_t)pt_ld * page_size >= (int64_t)b->max_ctx;
+}
+
 inline int ceil_div(int64_t a, int64_t b) { return (int)((a + b - 1) / b); }
 
 } // namespace janus

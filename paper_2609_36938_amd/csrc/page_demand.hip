@@ -291,7 +291,7 @@ extern "C" int janus_page_demand(const janus_batch *bt, const int32_t *topk_idx,
     if (workspace_bytes)
         *workspace_bytes = 0;
     if (!batch_ok(bt) || !topk_idx || !page_table || !bitmap || !page_list || !runs || !counts || k < 1 ||
-        pt_ld < 1 || !pow2(page_size) || num_phys_pages < 0 || max_run < 1)
+        pt_ld < 1 || !pow2(page_size) || !table_covers(bt, pt_ld, page_size) || num_phys_pages < 0 || max_run < 1)
         return JANUS_ERR_INVALID_ARG;
     if (num_phys_pages > PD_MAX_PAGES)
         return JANUS_ERR_UNSUPPORTED;

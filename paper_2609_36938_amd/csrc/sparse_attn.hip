@@ -789,7 +789,8 @@ static bool attn_args_ok(const janus_batch *bt, const void *q, int Hq, int dqk, 
                          int pt_ld, int page_size, const int32_t *topk_idx, int k, const void *out)
 {
     return batch_ok(bt) && q && k_pool && v_pool && page_table && topk_idx && out && Hq >= 1 && dqk >= 1 &&
-           dv >= 1 && k >= 1 && pt_ld >= 1 && pow2(page_size) && k_row_stride >= dqk && v_row_stride >= dv;
+           dv >= 1 && k >= 1 && pt_ld >= 1 && pow2(page_size) && table_covers(bt, pt_ld, page_size) &&
+           k_row_stride >= dqk && v_row_stride >= dv;
 }
 
 }  // namespace janus
@@ -852,7 +853,8 @@ extern "C" int janus_sparse_attn_fp8kv(const janus_batch *bt, const void *q, int
                                        void *stream)
 {
     if (!batch_ok(bt) || !q || !kv_pool || !page_table || !topk_idx || !out || !workspace_bytes || Hq < 1 ||
-        k < 1 || pt_ld < 1 || !pow2(page_size) || row_bytes < KV8_ROWB || num_splits < 0 ||
+        k < 1 || pt_ld < 1 || !pow2(page_size) || !table_covers(bt, pt_ld, page_size) || row_bytes < KV8_ROWB ||
+        num_splits < 0 ||
         num_splits > MAX_SPLITS)
         return JANUS_ERR_INVALID_ARG;
     if (out_dt != JANUS_BF16 && out_dt != JANUS_F32)

@@ -196,3 +196,46 @@ def test_fp8kv_attention_rejections(L):
     assert call(k=5000) == 2
     assert call(odt=2) == 2               # out dtype fp8
     assert call(q=ctypes.c_void_p(0x1008)) == 2  # misaligned q
+
+
+def test_page_table_narrower_than_the_context_is_rejected(L):
+    """Every call that reads a page table checks on the host that pt_ld pages
+    cover the longest session (max_ctx = 100 ids here: 2 pages of 64 do, 1
+    does not); a narrower table would be read past its end on the device."""
+    b = _batch()
+    ws = ctypes.c_size_t(0)
+    f = ctypes.c_float(0.1)
+    for pt_ld, want in ((1, 1), (2, 0)):
+        # page demand and unsplit attention launch once the table is wide
+        # enough, so only their rejection is exercised here
+        if want:
+            assert L.janus_page_demand(ctypes.byref(b), FAKE, 8, FAKE, pt_ld, 64, None, 100, 32, FAKE, FAKE, FAKE,
+                                       FAKE, None, ctypes.byref(ws), None) == 1
+            assert L.janus_sparse_attn(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 576, 576, FAKE, pt_ld, 64,
+                                       FAKE, 8, f, FAKE, 1, None, None) == 1
+        # the split and fp8-KV calls stop at their size query when the table is wide enough
+        rc = L.janus_sparse_attn_split(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 576, 576, FAKE, pt_ld, 64,
+                                       FAKE, 2048, f, FAKE, 1, None, 4, None, ctypes.byref(ws), None)
+        assert rc == want
+        rc = L.janus_sparse_attn_fp8kv(ctypes.byref(b), FAKE, 128, FAKE, 592, FAKE, pt_ld, 64, FAKE, 64, f, FAKE, 1,
+                                       None, 1, None, ctypes.byref(ws), None)
+        assert rc == want
+    # entries: max_ctx counts entries, so 1 page of 128 entries covers 100 of them
+    assert L.janus_sparse_attn_fp8kv(ctypes.byref(b), FAKE, 128, FAKE, 592, FAKE, 1, 128, FAKE, 64, f, FAKE, 1,
+                                     None, 1, None, ctypes.byref(ws), None) == 0
+
+
+def test_null_workspace_is_always_a_size_query(L):
+    """A NULL workspace only reports the size, also when 0 bytes are needed
+    (one slice): the call returns ok without launching (on this host, which has
+    no GPU, a launch would have returned JANUS_ERR_DEVICE)."""
+    b = _batch()
+    f = ctypes.c_float(0.1)
+    ws = ctypes.c_size_t(777)
+    assert L.janus_sparse_attn_fp8kv(ctypes.byref(b), FAKE, 128, FAKE, 592, FAKE, 4, 64, FAKE, 64, f, FAKE, 1,
+                                     None, 1, None, ctypes.byref(ws), None) == 0
+    assert ws.value == 0
+    ws = ctypes.c_size_t(777)
+    assert L.janus_sparse_attn_split(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 576, 576, FAKE, 4, 64, FAKE,
+                                     2048, f, FAKE, 1, None, 1, None, ctypes.byref(ws), None) == 0
+    assert ws.value == 0

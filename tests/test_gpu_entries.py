@@ -1,5 +1,5 @@
 """Entry granularity on the GPU against the oracle.  DeepSeek-V4 selects
-entries (Sec. 2.1 footnote), each one cached row standing for E = 128
+entries (Sec. 2.2 footnote), each one cached row standing for E = 128
 consecutive tokens that a token can select once all of them have arrived.
 
 Batches: a ragged prefill-shaped batch (one session with 2048 history entries,

@@ -1,4 +1,4 @@
-"""IndexShare (the GLM-5 series' layer grouping, Sec. 2.1): four consecutive
+"""IndexShare (the GLM-5 series' layer grouping, Sec. 2.2): four consecutive
 sparse-attention layers share one selection.  Only the first runs the indexer
 and top-k, and each layer attends over its own KV cache and queries with the
 shared ids.  The four layers' pools share the page table, so one page-demand
