@@ -310,6 +310,36 @@ int janus_sparse_attn_split(const janus_batch *b,
                             void *stream);
 
 /*
+ * janus_sparse_attn_split without a workspace argument, for callers that
+ * cannot allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation).  Same arguments (minus workspace
+ * and workspace_bytes), same kernels and the same result as
+ * janus_sparse_attn_split with the same num_splits.  The slices' partial
+ * results go to a scratch array inside the library instead: one array of
+ * JANUS_NOALLOC_SCRATCH_BYTES per GPU the call runs on, held until the
+ * process ends, its address looked up on the first call on each device (the
+ * call allocates nothing and needs no initialisation).
+ *   - A launch needing more than JANUS_NOALLOC_SCRATCH_BYTES
+ *     (total_q * splits * Hq * 514 * 4 bytes, 0 for one slice) returns
+ *     JANUS_ERR_WORKSPACE and enqueues nothing.  With num_splits = 0 on a GPU
+ *     of 256 compute units and Hq <= 128 it always fits.
+ *   - Every call on one GPU shares that GPU's array: calls that may overlap
+ *     in time on one GPU (different streams, different host threads) race
+ *     and must be serialised by the caller.  Calls on one stream are fine.
+ *   - With more than one slice, out must be 16-byte aligned.
+ */
+#define JANUS_NOALLOC_SCRATCH_BYTES ((size_t)128 << 20)
+
+int janus_sparse_attn_split_noalloc(const janus_batch *b,
+                                    const void *q, int Hq, int dqk, int dv,
+                                    const void *k_pool, const void *v_pool,
+                                    int64_t k_row_stride, int64_t v_row_stride,
+                                    const int32_t *page_table, int pt_ld, int page_size,
+                                    const int32_t *topk_idx, int k, float softmax_scale,
+                                    void *out, janus_dtype out_dt, float *lse,
+                                    int num_splits, void *stream);
+
+/*
  * Sparse MLA attention over a KV cache stored in FP8 (Sec. 5.1 keeps KV
  * states in FP8).  The same attention as janus_sparse_attn with dqk = 576
  * and dv = 512, where every cached row is

@@ -65,9 +65,11 @@ def lib():
         L.janus_sparse_attn_split.argtypes = [BP, P, i32, i32, i32, P, P, i64, i64, P, i32, i32, P, i32, f32, P,
                                               i32, P, i32, P, SZ, P]
         L.janus_sparse_attn_fp8kv.argtypes = [BP, P, i32, P, i64, P, i32, i32, P, i32, f32, P, i32, P, i32, P, SZ, P]
+        L.janus_sparse_attn_split_noalloc.argtypes = [BP, P, i32, i32, i32, P, P, i64, i64, P, i32, i32, P, i32, f32,
+                                                      P, i32, P, i32, P]
         for f in ("janus_index_scores", "janus_topk", "janus_topk_sharded", "janus_page_demand",
                   "janus_predict_diff", "janus_sparse_attn", "janus_sparse_attn_split", "janus_index_scores_mxfp4",
-                  "janus_sparse_attn_fp8kv"):
+                  "janus_sparse_attn_fp8kv", "janus_sparse_attn_split_noalloc"):
             getattr(L, f).restype = ctypes.c_int
         L.janus_status_string.argtypes = [ctypes.c_int]
         L.janus_status_string.restype = ctypes.c_char_p
@@ -285,6 +287,31 @@ def sparse_attn_split(batch: Batch, q, k_pool, v_pool, page_table, page_size: in
     have = ctypes.c_size_t(workspace.numel() * workspace.element_size())
     rc = lib().janus_sparse_attn_split(*args, _ptr(workspace), ctypes.byref(have), _stream(stream))
     _check(rc, "janus_sparse_attn_split")
+    return out, lse
+
+
+def sparse_attn_split_noalloc(batch: Batch, q, k_pool, v_pool, page_table, page_size: int, topk_idx, scale: float,
+                              num_splits: int = 0, k_row_stride: Optional[int] = None,
+                              v_row_stride: Optional[int] = None, dv: Optional[int] = None, out_dtype: str = "bf16",
+                              want_lse: bool = False, out=None, lse=None, stream=None):
+    """janus_sparse_attn_split_noalloc: as sparse_attn_split, with the slices'
+    partial results in the library's own per-GPU scratch array instead of a
+    workspace (pass out, and lse if wanted, to allocate nothing here either);
+    returns (out, lse or None)."""
+    Hq, dqk = int(q.shape[-2]), int(q.shape[-1])
+    krs = int(k_row_stride if k_row_stride is not None else k_pool.shape[-1])
+    vrs = int(v_row_stride if v_row_stride is not None else v_pool.shape[-1])
+    dv = int(dv if dv is not None else (v_pool.shape[-1] if v_pool is not k_pool else dqk))
+    odt = {"bf16": (JANUS_BF16, torch.bfloat16), "f32": (JANUS_F32, torch.float32)}[out_dtype]
+    if out is None:
+        out = torch.empty((batch.total_q, Hq, dv), dtype=odt[1], device=q.device)
+    if want_lse and lse is None:
+        lse = torch.empty((batch.total_q, Hq), dtype=torch.float32, device=q.device)
+    rc = lib().janus_sparse_attn_split_noalloc(batch.ref, _ptr(q), Hq, dqk, dv, _ptr(k_pool), _ptr(v_pool), krs, vrs,
+                                               _ptr(page_table), _table(batch, page_table, page_size),
+                                               int(page_size), _ptr(topk_idx), int(topk_idx.shape[1]), float(scale),
+                                               _ptr(out), odt[0], _ptr(lse), int(num_splits), _stream(stream))
+    _check(rc, "janus_sparse_attn_split_noalloc")
     return out, lse
 
 

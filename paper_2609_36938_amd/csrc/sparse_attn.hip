@@ -24,6 +24,7 @@
 #include "janus_host.hpp"
 
 #include <algorithm>
+#include <mutex>
 #include <type_traits>
 
 namespace janus {
@@ -730,6 +731,31 @@ static void launch_mla(const janus_batch *bt, const void *q, int Hq, const void 
     }
 }
 
+// Slices per row: as given, or (0) enough for one block per compute unit (a
+// block fills a CU's LDS, so more slices only queue a second round), at most
+// one slice per 32-id tile and MAX_SPLITS.  Only the automatic count asks the
+// device.
+static int mla_split_count(const janus_batch *bt, int k, int num_splits, int *splits)
+{
+    int sp = num_splits;
+    if (sp == 0) {
+        int dev = 0, cus = 256;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+            return JANUS_ERR_DEVICE;
+        const int tq = std::max(bt->total_q, 1);
+        sp = std::min(MAX_SPLITS, std::max(1, (cus + tq - 1) / tq));
+    }
+    *splits = std::min(sp, (k + MLA_KT - 1) / MLA_KT);
+    return JANUS_OK;
+}
+
+// Workspace bytes of a split launch: each slice's unnormalised O, max and sum.
+static size_t mla_split_bytes(const janus_batch *bt, int Hq, int splits)
+{
+    return splits > 1 ? (size_t)bt->total_q * splits * Hq * (MLA_DV + 2) * sizeof(float) : (size_t)0;
+}
+
 // The MLA kernel over a whole or sliced selection (see janus_sparse_attn_split
 // for the slice count and workspace rules).
 template <bool KV8>
@@ -738,21 +764,10 @@ static int run_mla(const janus_batch *bt, const void *q, int Hq, const void *poo
                    void *out, janus_dtype out_dt, float *lse, int num_splits, void *workspace,
                    size_t *workspace_bytes, void *stream)
 {
-    // slices: as given, or (0) enough for one block per compute unit (a
-    // block fills a CU's LDS, so more slices only queue a second round), at
-    // most one slice per 32-id tile and MAX_SPLITS
-    int splits = num_splits;
-    if (splits == 0) {
-        int dev = 0, cus = 256;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
-            return JANUS_ERR_DEVICE;
-        const int tq = std::max(bt->total_q, 1);
-        splits = std::min(MAX_SPLITS, std::max(1, (cus + tq - 1) / tq));
-    }
-    splits = std::min(splits, (k + MLA_KT - 1) / MLA_KT);
-    const size_t need =
-        splits > 1 ? (size_t)bt->total_q * splits * Hq * (MLA_DV + 2) * sizeof(float) : (size_t)0;
+    int splits = 1;
+    if (const int rc = mla_split_count(bt, k, num_splits, &splits); rc != JANUS_OK)
+        return rc;
+    const size_t need = mla_split_bytes(bt, Hq, splits);
     if (!workspace) {
         *workspace_bytes = need;
         return JANUS_OK;
@@ -865,4 +880,68 @@ extern "C" int janus_sparse_attn_fp8kv(const janus_batch *bt, const void *q, int
         return JANUS_ERR_UNSUPPORTED;
     return run_mla<true>(bt, q, Hq, kv_pool, row_bytes, page_table, pt_ld, page_size, topk_idx, k, scale, out,
                          out_dt, lse, num_splits, workspace, workspace_bytes, stream);
+}
+
+// ---------------------------------------------------------------------------
+// Split attention without a caller workspace: the slices' partial results go
+// to a static device array of this library (one per GPU, kept until the
+// process ends).  Its address is taken once per device, with that device
+// current, on the entry point's first call there; the array's own name is a
+// host-side stand-in that must never reach a kernel.
+namespace janus {
+
+constexpr size_t NOALLOC_SCRATCH_BYTES = size_t(128) << 20;  // JANUS_NOALLOC_SCRATCH_BYTES
+constexpr int NOALLOC_MAX_DEVICES = 64;
+static_assert(NOALLOC_SCRATCH_BYTES == JANUS_NOALLOC_SCRATCH_BYTES, "header and library disagree");
+
+static __device__ __align__(256) uint8_t scratch[NOALLOC_SCRATCH_BYTES];
+
+static std::mutex g_scratch_mu;
+static void *g_scratch_dev[NOALLOC_MAX_DEVICES];  // device address of scratch, per device
+
+// This device's copy of the scratch array (its device address), looked up
+// on the first call on the device.
+static int device_scratch(void **ptr)
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= NOALLOC_MAX_DEVICES)
+        return JANUS_ERR_DEVICE;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_dev[dev]) {
+        void *p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p)
+            return JANUS_ERR_DEVICE;
+        g_scratch_dev[dev] = p;
+    }
+    *ptr = g_scratch_dev[dev];
+    return JANUS_OK;
+}
+
+}  // namespace janus
+
+extern "C" int janus_sparse_attn_split_noalloc(const janus_batch *bt, const void *q, int Hq, int dqk, int dv,
+                                               const void *k_pool, const void *v_pool, int64_t k_row_stride,
+                                               int64_t v_row_stride, const int32_t *page_table, int pt_ld,
+                                               int page_size, const int32_t *topk_idx, int k, float scale, void *out,
+                                               janus_dtype out_dt, float *lse, int num_splits, void *stream)
+{
+    if (!attn_args_ok(bt, q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, page_table, pt_ld, page_size,
+                      topk_idx, k, out) ||
+        num_splits < 0 || num_splits > MAX_SPLITS)
+        return JANUS_ERR_INVALID_ARG;
+    if (out_dt != JANUS_BF16 && out_dt != JANUS_F32)
+        return JANUS_ERR_UNSUPPORTED;
+    if (!mla_shape(q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, k))
+        return JANUS_ERR_UNSUPPORTED;
+    int splits = 1;
+    if (const int rc = mla_split_count(bt, k, num_splits, &splits); rc != JANUS_OK)
+        return rc;
+    size_t cap = NOALLOC_SCRATCH_BYTES;
+    if (mla_split_bytes(bt, Hq, splits) > cap)
+        return JANUS_ERR_WORKSPACE;
+    void *ws = nullptr;
+    if (const int rc = device_scratch(&ws); rc != JANUS_OK)
+        return rc;
+    return run_mla<false>(bt, q, Hq, k_pool, 2 * k_row_stride, page_table, pt_ld, page_size, topk_idx, k, scale, out,
+                          out_dt, lse, num_splits, ws, &cap, stream);
 }

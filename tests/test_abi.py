@@ -239,3 +239,20 @@ def test_null_workspace_is_always_a_size_query(L):
     assert L.janus_sparse_attn_split(ctypes.byref(b), FAKE, 128, 576, 512, FAKE, FAKE, 576, 576, FAKE, 4, 64, FAKE,
                                      2048, f, FAKE, 1, None, 1, None, ctypes.byref(ws), None) == 0
     assert ws.value == 0
+
+
+def test_noalloc_split_attention_host_checks(L):
+    """janus_sparse_attn_split_noalloc refuses, before touching a device, a
+    launch whose slice partials exceed its scratch array, and argument errors."""
+    f = ctypes.c_float(0.1)
+
+    def call(b, nsplit, Hq=128, dqk=576, pt_ld=4096, k=2048):
+        return L.janus_sparse_attn_split_noalloc(ctypes.byref(b), FAKE, Hq, dqk, 512, FAKE, FAKE, 576, 576, FAKE,
+                                                 pt_ld, 64, FAKE, k, f, FAKE, 1, None, nsplit, None)
+
+    big = _batch(total_q=2048)
+    assert 2048 * 16 * 128 * 514 * 4 > (128 << 20)
+    assert call(big, 16) == 3                      # JANUS_ERR_WORKSPACE: more than the scratch holds
+    assert call(big, 17) == 1 and call(big, -1) == 1
+    assert call(big, 2, dqk=128) == 2              # only the MLA shape splits
+    assert call(_batch(max_ctx=100), 2, pt_ld=1) == 1  # page table narrower than the context
