@@ -89,12 +89,27 @@ constexpr int KV8_TILE_CH = MLA_KT * KV8_CPR + KV8_GAP;  // 1192
 constexpr int KV8_SCALE = MLA_DQK;                       // byte of the scale in a row
 JANUS_DEV int kv8_key_off(int r) { return r * KV8_ROWB + (r >= 16 ? KV8_GAP * 16 : 0); }
 
+// bf16 rows in a tile buffer: dims 0..511 of key row r ("main", 1 KB) at
+// r * MLA_ROWB, so that one gather instruction loads one row and its source
+// row is wave-uniform; dims 512..575 of the 32 rows ("tail", 4 KB) after
+// them, in four 1 KB blocks of eight rows, one gather instruction each.  In
+// tail block m, row r (= 8m + i) and chunk cc (dims 512 + 8cc ..) sit at
+// 16-byte slot 8*(cc ^ m) + (i ^ cc): the 16 rows of one K-operand read then
+// fall in 16 different 16-byte bank groups.
+constexpr int MLA_TAIL = MLA_KT * MLA_ROWB;      // 37888
+constexpr int MLA_BUF16 = MLA_TAIL + 4 * 1024;   // 41984
+JANUS_DEV int tail_off(int r, int cc)
+{
+    const int m = r >> 3;
+    return MLA_TAIL + 1024 * m + 16 * (8 * (cc ^ m) + ((r & 7) ^ cc));
+}
+
 template <bool KV8>
 constexpr int mla_tile_ch() { return KV8 ? KV8_TILE_CH : MLA_TILE_CH; }
 template <int NW, bool KV8>
 constexpr int mla_ipw() { return ((mla_tile_ch<KV8>() + 63) / 64 + NW - 1) / NW; }
 template <int NW, bool KV8>
-constexpr int mla_buf_bytes() { return NW * mla_ipw<NW, KV8>() * 64 * 16; }
+constexpr int mla_buf_bytes() { return KV8 ? NW * mla_ipw<NW, KV8>() * 64 * 16 : MLA_BUF16; }
 
 // Tile chunk 64*j + lane (j wave-uniform) -> key row r and chunk c of that
 // row.  Chunks that are not part of a row (bf16 row padding, the fp8 gap)
@@ -210,9 +225,9 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     __syncthreads();
 
     const int ntiles = (kl + MLA_KT - 1) / MLA_KT;
-    // gather of tile t: the wave's instruction i fills LDS chunks 64j .. 64j+63,
-    // j = wave + NW*i (chunks 72 and 73 of each row are padding and load a
-    // dummy; padding ids load row 0; slots past the tile load a dummy too)
+    // ---- fp8 rows: gather of tile t: the wave's instruction i fills LDS
+    // chunks 64j .. 64j+63, j = wave + NW*i (chunks of the gap load a dummy;
+    // padding ids load row 0; slots past the tile load a dummy too)
     auto issue = [&](int t, int i0, int i1, uint8_t *__restrict__ dst) {
 #pragma unroll 1
         for (int i = i0; i < i1; ++i) {
@@ -253,12 +268,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
         }
     };
-    // the gathers of tile t+2 go out in five groups inside the S loop (at
-    // K-steps 0, 4, 8, 12 and 16; with eight waves one instruction each, with
-    // four two), so that an issue stalled behind the gather queue overlaps
-    // MFMAs already in flight instead of holding every wave at the top of
-    // the step; other wave counts issue them all at step 0
-    constexpr bool SPREAD = IPW == 5 || IPW == 10 || (KV8 && IPW >= 2);
+    constexpr bool SPREAD8 = KV8 && IPW >= 2;
     auto spread_part = [&](auto Qc, int t, uint8_t *__restrict__ dst) {
         constexpr int Q = decltype(Qc)::value;
         constexpr int I0 = IPW <= 5 ? Q : Q * IPW / 5;
@@ -266,9 +276,90 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         if constexpr (I1 > I0)
             issue_group(std::integral_constant<int, I0>{}, std::integral_constant<int, I1>{}, t, dst);
     };
-    auto issue_part = [&](int t, int part, uint8_t *__restrict__ dst) {
-        if (t + 2 < ntiles) {
-            if constexpr (SPREAD) {
+
+    // ---- bf16 rows: wave w gathers main rows MROWS*w .. MROWS*w+MROWS-1
+    // (one instruction each: a wave-uniform source row, its slot taken from
+    // a register of prefetched slots) and tail blocks m = w + NW*u < 4
+    constexpr int MROWS = MLA_KT / NW;
+    constexpr int NTAIL = NW >= 4 ? 1 : 4 / NW;
+    const bool has_tail = wave < 4;  // (every wave when NW <= 4)
+    // the row and chunk tail block m's lane loads
+    auto tail_rc = [&](int m, int ln, int &r, int &cc) {
+        cc = (ln >> 3) ^ m;
+        r = 8 * m + ((ln & 7) ^ cc);
+    };
+    // slots of tile tt: lane l < 32 (and l - 32) holds row l's, ts[u] the
+    // one of the row this lane loads in tail block wave + NW*u
+    auto read_slots = [&](int tt, int &vs, int (&ts)[NTAIL]) {
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        vs = sSlot[min(MLA_KT * tt + (ln & 31), kl - 1)];
+#pragma unroll
+        for (int u = 0; u < NTAIL; ++u) {
+            int r, cc;
+            tail_rc(min(wave + NW * u, 3), ln, r, cc);
+            ts[u] = sSlot[min(MLA_KT * tt + r, kl - 1)];
+        }
+    };
+    // main row i of this wave for tile tt
+    auto fire_main = [&](int i, int tt, int vs, uint8_t *__restrict__ dst) {
+        const int r = MROWS * wave + i;
+        int sl = __builtin_amdgcn_readlane(vs, r);
+        if (MLA_KT * tt + r >= kl || sl < 0)
+            sl = 0;  // padding rows read a real row; their logits are masked
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+        const uint8_t *src = kv + (uint64_t)(uint32_t)sl * (uint32_t)row_bytes + 16 * ln;
+        __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + r * MLA_ROWB), 16, 0, 0);
+    };
+    auto fire_tails = [&](int tt, const int (&ts)[NTAIL], uint8_t *__restrict__ dst) {
+        int ln = lane;
+        asm volatile("" : "+v"(ln));
+#pragma unroll
+        for (int u = 0; u < NTAIL; ++u) {
+            const int m = wave + NW * u;
+            int r, cc;
+            tail_rc(m, ln, r, cc);
+            const int sl = (MLA_KT * tt + r < kl && ts[u] >= 0) ? ts[u] : 0;
+            const uint8_t *src = kv + (uint64_t)(uint32_t)sl * (uint32_t)row_bytes + 16 * (64 + cc);
+            __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + MLA_TAIL + 1024 * m), 16, 0,
+                                             0);
+        }
+    };
+    // all of tile tt's gathers at once (the first two tiles)
+    auto issue_all = [&](int tt, uint8_t *__restrict__ dst) {
+        if constexpr (KV8) {
+            issue(tt, 0, IPW, dst);
+        } else {
+            int vs, ts[NTAIL];
+            read_slots(tt, vs, ts);
+#pragma unroll 1
+            for (int i = 0; i < MROWS; ++i)
+                fire_main(i, tt, vs, dst);
+            if (has_tail)
+                fire_tails(tt, ts, dst);
+        }
+    };
+    // wait until this wave's gathers of the tile before the newest one
+    // have landed (pending: the newest tile's are in flight)
+    auto wait_gathers = [&](bool pending) {
+        if (!pending)
+            __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+        else if constexpr (KV8)
+            __builtin_amdgcn_s_waitcnt(vmcnt_only(IPW));
+        else if (has_tail)
+            __builtin_amdgcn_s_waitcnt(vmcnt_only(MROWS + NTAIL));
+        else
+            __builtin_amdgcn_s_waitcnt(vmcnt_only(MROWS));
+    };
+    // issue point q (0..4) inside tile t's S loop, for the gathers of tile
+    // t+2: bf16 main rows in four parts, then the tails; fp8 in five groups
+    // (with eight waves one instruction each) or all at point 0
+    auto issue_part = [&](int t, int part, int vs, const int (&ts)[NTAIL], uint8_t *__restrict__ dst) {
+        if (t + 2 >= ntiles)
+            return;
+        if constexpr (KV8) {
+            if constexpr (SPREAD8) {
                 switch (part) {
                 case 0: spread_part(std::integral_constant<int, 0>{}, t + 2, dst); break;
                 case 1: spread_part(std::integral_constant<int, 1>{}, t + 2, dst); break;
@@ -280,9 +371,24 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             } else if (part == 0) {
                 issue(t + 2, 0, IPW, dst);
             }
+        } else if (part < 4) {
+#pragma unroll
+            for (int i = part * MROWS / 4; i < (part + 1) * MROWS / 4; ++i)
+                fire_main(i, t + 2, vs, dst);
+        } else if (has_tail) {
+            fire_tails(t + 2, ts, dst);
         }
     };
     auto tile_step = [&](int t, const uint8_t *__restrict__ tile, uint8_t *__restrict__ next) {
+        // slots of tile t+2's gathers (bf16), read now so that their LDS
+        // latency passes under the first K-steps (rows past the selection
+        // read a clamped slot and are redirected when their gather fires)
+        int vs = 0, ts[NTAIL];
+#pragma unroll
+        for (int u = 0; u < NTAIL; ++u)
+            ts[u] = 0;
+        if constexpr (!KV8)
+            read_slots(t + 2, vs, ts);
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
         v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
         // K operands: 16 bytes (bf16) or 8 bytes (fp8, widened to bf16 in
@@ -306,19 +412,32 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // or softmax VALU work (measured 3% faster; no gain with bf16 rows)
         if constexpr (KV8)
             __builtin_amdgcn_s_setprio(1);
+        // K operand of a step for keys c16 (h = 0) and c16 + 16 (h = 1): bf16
+        // steps 16 and 17 (dims 512..575) come from the tail blocks
+        // (tail addresses from an opaque copy of the lane index, so that the
+        // compiler computes them here instead of keeping them for the whole loop)
+        int lnk = lane;
+        asm volatile("" : "+v"(lnk));
+        auto kop = [&](int step, int h) -> KRaw {
+            if (!KV8 && step >= 16)
+                return *(const KRaw *)(tile + tail_off((lnk & 15) + 16 * h, 4 * (step - 16) + (lnk >> 4)));
+            return *(const KRaw *)((h ? row1 : row0) + SB * step);
+        };
         KRaw ring[2][2];
-        ring[0][0] = *(const KRaw *)row0;
-        ring[0][1] = *(const KRaw *)row1;
+        ring[0][0] = kop(0, 0);
+        ring[0][1] = kop(0, 1);
 #pragma unroll
         for (int step = 0; step < MLA_STEPS; ++step) {
             if (step + 1 < MLA_STEPS) {
-                ring[(step + 1) & 1][0] = *(const KRaw *)(row0 + SB * (step + 1));
-                ring[(step + 1) & 1][1] = *(const KRaw *)(row1 + SB * (step + 1));
+                ring[(step + 1) & 1][0] = kop(step + 1, 0);
+                ring[(step + 1) & 1][1] = kop(step + 1, 1);
             }
             st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step & 1][0]), qf[step], st0, 0, 0, 0);
             st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step & 1][1]), qf[step], st1, 0, 0, 0);
-            if (step % 4 == 0)
-                issue_part(t, step / 4, next);
+            // issue points: fp8 at steps 0, 4, .., 16; bf16 at 2, 6, 10, 14
+            // and 17, after the slots read at the top of the tile have landed
+            if (KV8 ? step % 4 == 0 : (step % 4 == 2 || step == MLA_STEPS - 1))
+                issue_part(t, KV8 ? step / 4 : (step == MLA_STEPS - 1 ? 4 : step / 4), vs, ts, next);
             __builtin_amdgcn_sched_barrier(0);
         }
         if constexpr (KV8)
@@ -444,21 +563,15 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             __builtin_amdgcn_s_setprio(0);
         // tile t+1 has landed once at most tile t+2's gathers are pending; the
         // barrier also frees this tile's buffer for the gather of tile t+3
-        if (t + 2 < ntiles)
-            __builtin_amdgcn_s_waitcnt(vmcnt_only(IPW));
-        else
-            __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+        wait_gathers(t + 2 < ntiles);
         lds_barrier();
     };
 
     if (ntiles > 0)
-        issue(0, 0, IPW, sKV0);
+        issue_all(0, sKV0);
     if (ntiles > 1)
-        issue(1, 0, IPW, sKV1);
-    if (ntiles > 1)
-        __builtin_amdgcn_s_waitcnt(vmcnt_only(IPW));
-    else
-        __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+        issue_all(1, sKV1);
+    wait_gathers(ntiles > 1);
     __syncthreads();
     for (int t = 0; t < ntiles; ++t) {
         const int r3 = t % 3;
