@@ -389,6 +389,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             ts[u] = 0;
         if constexpr (!KV8)
             read_slots(t + 2, vs, ts);
+        int vslot;
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
         v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
         // K operands: 16 bytes (bf16) or 8 bytes (fp8, widened to bf16 in
@@ -438,6 +439,9 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             // and 17, after the slots read at the top of the tile have landed
             if (KV8 ? step % 4 == 0 : (step % 4 == 2 || step == MLA_STEPS - 1))
                 issue_part(t, KV8 ? step / 4 : (step == MLA_STEPS - 1 ? 4 : step / 4), vs, ts, next);
+            // this tile's slots (for its valid keys), read under the last MFMAs
+            if (step == MLA_STEPS - 1)
+                vslot = sSlot[min(MLA_KT * t + (lane & 31), kl - 1)];
             __builtin_amdgcn_sched_barrier(0);
         }
         if constexpr (KV8)
@@ -445,8 +449,12 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // online softmax (exp2 domain) with lazy rescaling of O.  Valid keys
         // of the tile come as a 32-bit mask (lanes 32-63 repeat 0-31); this
         // lane's keys are 16*kb + 4*grp + i
-        const int vkey = MLA_KT * t + (lane & 31);
-        const uint32_t vmask = (uint32_t)__ballot(vkey < kl && sSlot[vkey] >= 0) >> (4 * grp);
+        const uint32_t vbits = (uint32_t)__ballot(MLA_KT * t + (lane & 31) < kl && vslot >= 0);
+        const uint32_t vmask = vbits >> (4 * grp);
+        // the common case - every key of the tile valid, bf16 rows and a
+        // positive scale - takes the max over the raw products and one fma
+        // per probability, with no masks
+        const bool fast = !KV8 && vbits == 0xFFFFFFFFu && scale_log2 > 0.f;
         // fp8 rows: each key's scale multiplies its logit and its probability
         float ks[2][4];
         if constexpr (KV8) {
@@ -458,15 +466,20 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         }
         float x[2][4];
         float mx = -INFINITY;
+        if (fast) {
+            mx = scale_log2 * fmaxf(fmaxf(fmaxf(st0[0], st0[1]), fmaxf(st0[2], st0[3])),
+                                    fmaxf(fmaxf(st1[0], st1[1]), fmaxf(st1[2], st1[3])));
+        } else {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const bool ok = (vmask >> (16 * kb + i)) & 1u;
-                const float sc = KV8 ? scale_log2 * ks[kb][i] : scale_log2;
-                x[kb][i] = ok ? (kb ? st1[i] : st0[i]) * sc : -INFINITY;
-                mx = fmaxf(mx, x[kb][i]);
-            }
+                for (int i = 0; i < 4; ++i) {
+                    const bool ok = (vmask >> (16 * kb + i)) & 1u;
+                    const float sc = KV8 ? scale_log2 * ks[kb][i] : scale_log2;
+                    x[kb][i] = ok ? (kb ? st1[i] : st0[i]) * sc : -INFINITY;
+                    mx = fmaxf(mx, x[kb][i]);
+                }
+        }
         // the running max m is common to a head's four lane groups; it only
         // moves when some key exceeds it by the slack, which is rare after
         // the first tiles, so the cross-lane reduction runs only then
@@ -486,15 +499,26 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         if (lane == 0)
             sResc[wave] = resc;
         float pv[2][4];
+        if (fast) {
+            // m is finite here: a finite max has just been taken
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                pv[kb][i] = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[kb][i] - m);
-                lsum += pv[kb][i];
-                if constexpr (KV8)  // V_s = scale_s * (stored row); padding keys stay 0
-                    pv[kb][i] = ((vmask >> (16 * kb + i)) & 1u) ? pv[kb][i] * ks[kb][i] : 0.f;
-            }
+                for (int i = 0; i < 4; ++i) {
+                    pv[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(kb ? st1[i] : st0[i], scale_log2, -m));
+                    lsum += pv[kb][i];
+                }
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    pv[kb][i] = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[kb][i] - m);
+                    lsum += pv[kb][i];
+                    if constexpr (KV8)  // V_s = scale_s * (stored row); padding keys stay 0
+                        pv[kb][i] = ((vmask >> (16 * kb + i)) & 1u) ? pv[kb][i] * ks[kb][i] : 0.f;
+                }
+        }
         const v8bf pa = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
                              (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
         sP[64 * wave + lane] = __builtin_bit_cast(v4i, pa);
@@ -505,6 +529,12 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // 16*hb + c16; slots: keys 4*grp + i and 16 + 4*grp + i).  V operand:
         // those keys, lane (r' = c16/4, cc = c16%4) addressing dims
         // 16*nb + 4*cc .. +3 of its key row
+        // head blocks rescaled this tile (wave-uniform), read before the V
+        // operands so that waiting for them does not wait for those
+        uint32_t rmask = 0;
+#pragma unroll
+        for (int hb = 0; hb < NW; ++hb)
+            rmask |= (sResc[hb] != 0 ? 1u : 0u) << hb;
         v8bf bv[NBW];
         if constexpr (KV8) {
             // fp8 rows: lane (c16, grp) addresses key j = c16/2 of the P
@@ -531,11 +561,6 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         }
         if constexpr (KV8)
             __builtin_amdgcn_s_setprio(1);
-        // head blocks rescaled this tile, read together (wave-uniform)
-        uint32_t rmask = 0;
-#pragma unroll
-        for (int hb = 0; hb < NW; ++hb)
-            rmask |= (sResc[hb] != 0 ? 1u : 0u) << hb;
         // P fragments one head block ahead
         v4i pf[2];
         pf[0] = sP[lane];
