@@ -14,8 +14,13 @@ A step is the whole path for the layer on one stream:
 value = appended tokens per second per layer (N * steps / time).
 
 Printed as one JSON line (see the keys below), with the roofline of the
-dominant kernel (index scores, fp8 MFMA) from HIP events on the launch stream,
-and the CPU oracle timed on a bounded row sample on the host cores.
+dominant kernel (index scores, fp8 MFMA) from HIP events on the launch stream
+(medians over the timed steps), and the CPU oracle timed on bounded row
+samples on the host cores, multi- and single-threaded.  Further fields (left
+out by --core-only): the attention with selections spread over the pool, the
+sharded-prediction sweep (Eq. 3) on workloads whose selection does not
+saturate, the predicted path of Eq. 2 over 8 layers of the prediction
+workload, the decode step, an IndexShare group and the attention over FP8 KV.
 """
 from __future__ import annotations
 
@@ -45,7 +50,10 @@ def parse():
     p.add_argument("--core-only", action="store_true",
                    help="time the one-layer step only: no sharded sweep, decode, IndexShare or fp8-KV fields "
                         "(for profiler passes)")
-    p.add_argument("--cpu-rows", type=int, default=128, help="query rows in the oracle's timed sample")
+    p.add_argument("--cpu-rows", type=int, default=128, help="query rows in the oracle's multi-threaded sample")
+    p.add_argument("--cpu-rows-1t", type=int, default=16, help="query rows in the oracle's single-threaded sample")
+    p.add_argument("--c4-layers", type=int, default=8,
+                   help="layers of the prediction workload (history 131072 + 4096) in the predicted-path field")
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "index_scores_traffic.json"))
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (known bytes) for HBM counter calibration")
@@ -144,7 +152,9 @@ def main():
     for e in evs:
         step(e)
     torch.cuda.synchronize()
-    per = {n: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, n in enumerate(names)}
+    # median over the timed steps (the mean is kept beside it)
+    per = {n: float(np.median([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, n in enumerate(names)}
+    per_mean = {n: float(np.mean([e[j].elapsed_time(e[j + 1]) for e in evs])) for j, n in enumerate(names)}
 
     # algorithmic work
     pairs = N * (M + 1) + N * (N - 1) // 2                  # causal (token, candidate) pairs
@@ -160,8 +170,9 @@ def main():
     ms_step = wall / args.steps * 1e3
     counts = diff_out[2].cpu().tolist()
     extras = not args.core_only
-    sharded = (sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, pd_out[0], pt, ps, P, mr, k)
-               if extras else None)
+    spread = spread_attention(janus, torch, wl, bt, qa, kv, pt, ai, max(args.steps, 5)) if extras else None
+    sweep = prediction_sweep(janus, torch, max(args.steps, 5)) if extras else None
+    predicted = predicted_path(janus, torch, args.c4_layers) if extras and args.c4_layers > 0 else None
     decode = decode_step(janus, torch, max(args.steps, 5)) if extras and not args.no_decode else None
     kv8 = fp8kv_attention(janus, torch, bt, qa, kv, pt, ps, sel, ai, max(args.steps, 5), per["sparse_attn"]) \
         if extras else None
@@ -188,6 +199,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": "index_scores", "achieved": ach / 1e12, "peak": PEAK_FP8 / 1e12,
                      "unit": "TFLOP/s", "frac": ach / PEAK_FP8, "traffic": traffic},
         "kernels_ms": per,
+        "kernels_ms_mean": per_mean,
         "kernel_rates": {
             "index_scores_TFLOPs": idx_flop / t_idx / 1e12,
             "topk_GBps": topk_bytes / (per["topk"] * 1e-3) / 1e9,
@@ -198,13 +210,16 @@ def main():
             "sparse_attn_frac_bf16_mfma": attn_flop / (per["sparse_attn"] * 1e-3) / PEAK_BF16,
         },
         "demand": {"pages": int(pd_out[3][0]), "runs": int(pd_out[3][1]), "pred_counts": counts},
-        "sharded_prediction": sharded,
+        "sparse_attn_spread": spread,
+        "prediction_sweep": sweep,
+        "predicted_path": predicted,
         "decode": decode,
         "indexshare": share,
         "fp8_kv": kv8,
     }
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows)
+        rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows, args.cpu_rows_1t, sel.cpu().numpy(),
+                                           pred_bm.cpu().numpy().view(np.uint32))
     print(json.dumps(rec))
 
 
@@ -266,26 +281,172 @@ def record_traffic(fetch_csv, write_csv, out_path):
     print(json.dumps(rec))
 
 
-def sharded_prediction(janus, torch, bt, qp, kI, w, sqp, sk, scores, actual_bm, pt, ps, P, mr, k):
-    """Synchronization-free sharded prediction (Eq. 3) of this layer's set from
-    the predicted queries, for several shard counts: the per-shard top-k time
-    (all shards on this GPU; one GPU's share is 1/G of it) and the recall and
-    precision of the predicted page set against the actual one."""
-    janus.index_scores(bt, qp, kI, w, q_scale=sqp, k_scale=sk, scores=scores)
-    res = {}
-    for G in (1, 2, 4, 8):
-        janus.topk_sharded(bt, scores, k, G, ps)  # warm
+def _pct(a, b):
+    return a / b if b else 1.0
+
+
+def spread_attention(janus, torch, wl, bt, qa, kv, pt, ai, steps):
+    """The 128K attention with selections spread over the whole causal range
+    (every row's 2048 ids uniform over its candidates, no hot spans), so that
+    the gathered rows cover the whole 160 MB pool instead of ~111 hot pages.
+    Same queries and pool as the step."""
+    from workloads import synth_topk
+    sel = torch.from_numpy(synth_topk(wl, seed=5, hot_frac=0.0)).to(qa.device)
+    out = torch.empty((bt.total_q, ai.Hq, ai.dv), dtype=torch.bfloat16, device=qa.device)
+    f = lambda: janus.sparse_attn(bt, qa, kv, kv, pt, wl.page_size, sel, ai.scale, dv=ai.dv, out=out)
+    f()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(steps):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        sel = janus.topk_sharded(bt, scores, k, G, ps)
+        f()
         e1.record()
-        bm = janus.page_demand(bt, sel, pt, ps, P, mr)[0]
-        c = janus.predict_diff(actual_bm, bm, P, mr)[2].cpu().tolist()
         torch.cuda.synchronize()
-        a, p, ap = c[0], c[1], c[2]
-        res[str(G)] = {"topk_ms": e0.elapsed_time(e1), "recall": ap / a if a else 1.0,
-                       "precision": ap / p if p else 1.0, "pred_pages": p, "miss_pages": c[3]}
-    return res
+        ts.append(e0.elapsed_time(e1))
+    ms = float(np.median(ts))
+    gather = bt.total_q * sel.shape[1] * ai.dqk * 2.0
+    return {"workload": "sparse attention of the 128K workload, each row's 2048 ids uniform over its causal "
+                        "range (the whole 160 MB pool is gathered)",
+            "ms": ms, "gather_GBps_logical": gather / (ms * 1e-3) / 1e9,
+            "gather_frac_hbm": gather / (ms * 1e-3) / PEAK_HBM}
+
+
+SWEEP_LAYOUTS = (("hot spans 1% of the history (fewer tokens than k), one in each eighth", 0.01, "even"),
+                 ("hot spans 5% of the history, all in its most recent quarter", 0.05, "recent"))
+
+
+def prediction_sweep(janus, torch, steps):
+    """Synchronization-free sharded prediction (Eq. 3) against the exact
+    selection, for G = 1, 2, 4, 8 history shards, on workloads where the
+    selection does not saturate: one session, history 131072, 64 appended
+    tokens, the 64 x 128 fp8 indexer, k = 2048, predicted queries
+    0.9 q + sqrt(0.19) N(0, 1).  Recall = |A & P| / |A| and precision =
+    |A & P| / |P| (Sec. 4.2) of the history sets, at token granularity and at
+    64-token pages (identity page table); the sharded top-k time is for all G
+    shards on this GPU (one GPU's share is 1/G of it)."""
+    from workloads import make_workload
+    dev = torch.device("cuda:0")
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    out = []
+    for name, frac, layout in SWEEP_LAYOUTS:
+        wl = make_workload(hist_len=[131072], new_len=[64], H=64, d=128, idx_dtype="fp8", k=2048, seed=7,
+                           w_scale=1.0 / 8, table="identity", q_pred_corr=0.9, hot_frac=frac, hot_layout=layout)
+        bt = janus.Batch(wl.hist_len, wl.new_len, device=dev)
+        kI, w, sk = T(wl.kI), T(wl.w), T(wl.k_scale)
+        M, ctx = int(wl.hist_len[0]), int(wl.ctx_len[0])
+        levels = {"token": (1, T(np.arange(ctx, dtype=np.int32)[None, :]), ctx),
+                  "page64": (64, T(wl.page_table), wl.num_phys_pages)}
+        sc = janus.index_scores(bt, T(wl.q), kI, w, q_scale=T(wl.q_scale), k_scale=sk)
+        sel = janus.topk(bt, sc, wl.k)
+        actual = {lv: janus.page_demand(bt, sel, tab, psz, npg, 32)[0].clone()
+                  for lv, (psz, tab, npg) in levels.items()}
+        janus.index_scores(bt, T(wl.q_pred), kI, w, q_scale=T(wl.q_pred_scale), k_scale=sk, scores=sc)
+        rows = {}
+        for G in (1, 2, 4, 8):
+            janus.topk_sharded(bt, sc, wl.k, G, 64)
+            ts = []
+            for _ in range(steps):
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                psel = janus.topk_sharded(bt, sc, wl.k, G, 64)
+                e1.record()
+                torch.cuda.synchronize()
+                ts.append(e0.elapsed_time(e1))
+            r = {"topk_sharded_ms": float(np.median(ts))}
+            for lv, (psz, tab, npg) in levels.items():
+                bm = janus.page_demand(bt, psel, tab, psz, npg, 32)[0]
+                c = janus.predict_diff(actual[lv], bm, npg, 32)[2].cpu().tolist()
+                r[lv] = {"actual": c[0], "predicted": c[1], "recall": _pct(c[2], c[0]),
+                         "precision": _pct(c[2], c[1]), "miss": c[3], "miss_runs": c[4]}
+            rows[str(G)] = r
+        out.append({"workload": name, "history": M, "new_tokens": int(wl.total_q), "k": wl.k, "shards": rows})
+        del sc, sel, kI
+    return out
+
+
+def predicted_path(janus, torch, layers):
+    """The prediction workload over several layers: history 131072 + 4096
+    appended tokens, the 64 x 128 fp8 indexer with the same hot-span positions
+    in every layer, k = 2048, identity page table, max run 32.  Per layer the
+    actual path (scores -> top-k -> page demand and runs -> sparse MLA
+    attention over the actual set) and the predicted path of Eq. 2 (scores ->
+    top-k -> page demand on q_pred = 0.9 q + sqrt(0.19) N(0, 1)) and the
+    corrective set (predict_diff).  Indexer inputs come from the shared
+    generator; attention queries and the KV pool of each layer are drawn on
+    the GPU from a seeded generator (nothing here is compared with the
+    oracle).  Times are medians of HIP-event timings over two passes."""
+    from workloads import config
+    dev = torch.device("cuda:0")
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    g = torch.Generator(device=dev)
+    g.manual_seed(4)
+    L = []
+    for layer in range(layers):
+        wl = config(4, layer=layer)
+        L.append(dict(q=T(wl.q), sq=T(wl.q_scale), qp=T(wl.q_pred), sqp=T(wl.q_pred_scale), kI=T(wl.kI),
+                      sk=T(wl.k_scale), w=T(wl.w),
+                      qa=torch.randn((wl.total_q, 128, 576), generator=g, device=dev).to(torch.bfloat16),
+                      kv=(torch.randn((wl.num_phys_pages * wl.page_size, 576), generator=g, device=dev)
+                          / 24.0).to(torch.bfloat16)))
+    bt = janus.Batch(wl.hist_len, wl.new_len, device=dev)
+    pt, P, ps, k, mr = T(wl.page_table), wl.num_phys_pages, wl.page_size, wl.k, wl.max_run
+    scores = torch.empty(bt.total_scores, dtype=torch.float32, device=dev)
+    sel = torch.empty((bt.total_q, k), dtype=torch.int32, device=dev)
+    psel = torch.empty_like(sel)
+    out = torch.empty((bt.total_q, 128, 512), dtype=torch.bfloat16, device=dev)
+    mk = lambda: (torch.empty((P + 31) // 32, dtype=torch.int32, device=dev),
+                  torch.empty(P, dtype=torch.int32, device=dev),
+                  torch.empty(2 * P, dtype=torch.int32, device=dev), torch.empty(2, dtype=torch.int32, device=dev))
+    pd_a, pd_p = mk(), mk()
+    diff = (torch.empty((P + 31) // 32, dtype=torch.int32, device=dev),
+            torch.empty(2 * P, dtype=torch.int32, device=dev), torch.empty(5, dtype=torch.int32, device=dev))
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    per_layer = []
+    for rep in range(2):
+        for li, x in enumerate(L):
+            e = [ev() for _ in range(10)]
+            e[0].record()
+            janus.index_scores(bt, x["q"], x["kI"], x["w"], q_scale=x["sq"], k_scale=x["sk"], scores=scores)
+            e[1].record()
+            janus.topk(bt, scores, k, out=sel)
+            e[2].record()
+            janus.page_demand(bt, sel, pt, ps, P, mr, out=pd_a)
+            e[3].record()
+            janus.sparse_attn(bt, x["qa"], x["kv"], x["kv"], pt, ps, sel, 1.0 / 24.0, dv=512, out=out)
+            e[4].record()
+            janus.index_scores(bt, x["qp"], x["kI"], x["w"], q_scale=x["sqp"], k_scale=x["sk"], scores=scores)
+            e[5].record()
+            janus.topk(bt, scores, k, out=psel)
+            e[6].record()
+            janus.page_demand(bt, psel, pt, ps, P, mr, out=pd_p)
+            e[7].record()
+            janus.predict_diff(pd_a[0], pd_p[0], P, mr, out=diff)
+            e[8].record()
+            torch.cuda.synchronize()
+            d = [e[j].elapsed_time(e[j + 1]) for j in range(8)]
+            c = diff[2].cpu().tolist()
+            if rep == 0:
+                per_layer.append({"t": [], "counts": c, "runs": int(pd_a[3][1])})
+            per_layer[li]["t"].append(d)
+    names = ["index_scores", "topk", "page_demand", "sparse_attn", "pred_index_scores", "pred_topk",
+             "pred_page_demand", "predict_diff"]
+    layers_out = []
+    for li, rec in enumerate(per_layer):
+        t = np.median(np.array(rec["t"]), axis=0)
+        actual, pred = float(t[0] + t[1] + t[2] + t[3]), float(t[4] + t[5] + t[6])
+        c = rec["counts"]
+        layers_out.append({"layer": li, "actual_path_ms": actual, "predicted_path_ms": pred,
+                           "predict_diff_ms": float(t[7]), "prediction_overhead": (pred + float(t[7])) / actual,
+                           "actual_pages": c[0], "predicted_pages": c[1], "recall": _pct(c[2], c[0]),
+                           "precision": _pct(c[2], c[1]), "miss_pages": c[3], "miss_runs": c[4],
+                           "actual_runs": rec["runs"], "kernels_ms": dict(zip(names, map(float, t)))})
+    mean = lambda key: float(np.mean([r[key] for r in layers_out]))
+    return {"workload": f"{layers} layers, history 131072 + 4096 new tokens, k=2048, identity page table, "
+                        "q_pred = 0.9 q + sqrt(0.19) N(0,1)",
+            "per_layer_actual_ms": mean("actual_path_ms"), "per_layer_predicted_ms": mean("predicted_path_ms"),
+            "per_layer_predict_diff_ms": mean("predict_diff_ms"),
+            "prediction_overhead": mean("prediction_overhead"), "layers": layers_out}
 
 
 def fp8kv_attention(janus, torch, bt, qa, kv, pt, ps, sel, ai, steps, bf16_ms):
@@ -426,24 +587,72 @@ def decode_step(janus, torch, steps):
     }
 
 
-def cpu_baseline(wl, ai, nrows):
-    """The oracle, untuned, on a stride sample of query rows: scores, top-k and
-    attention for each sampled row (page demand is negligible beside them)."""
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(wl, ai, nrows, nrows_1t, gpu_sel, pred_bm):
+    """The oracle, untuned, on stride samples of query rows of the same
+    workload: scores over all candidates, top-k and attention for each sampled
+    row, timed stage by stage; page demand, runs and the corrective set over
+    the full selection (the GPU's ids, as in the parity tests).  Run with this
+    process's OpenMP thread count (OMP_NUM_THREADS, else the CPUs this
+    process may use) and again single-threaded on a smaller sample.
+    tokens/s = 1 / (row-stage seconds per row + set-stage seconds / N)."""
+    import ctypes
+
     import oracle
     from workloads import attention_q_rows
 
-    rows = np.linspace(0, wl.total_q - 1, nrows).astype(np.int32)
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    t0 = time.perf_counter()
-    sc = oracle.index_scores(wl.q_start, wl.hist_len, wl.q, "fp8", wl.q_scale, wl.kI, "fp8", wl.k_scale, wl.w, rows)
-    sel = oracle.topk(wl.q_start, wl.hist_len, rows, sc.astype(np.float32), wl.k)
-    qr = attention_q_rows(wl, rows)
-    oracle.sparse_attn(wl.q_start, wl.hist_len, rows, qr, ai.k_pool, None, ai.k_row_stride, ai.v_row_stride,
-                       wl.page_table, wl.page_size, sel, ai.scale, ai.dv)
-    dt = time.perf_counter() - t0
-    return {"value": nrows / dt, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{nrows} evenly spaced query rows of the same workload (scores over all "
-                      f"~139K candidates, top-k, attention over k=2048); {dt:.1f} s"}
+    oracle.lib()
+    gomp = ctypes.CDLL("libgomp.so.1")
+    threads = int(os.environ.get("OMP_NUM_THREADS") or len(os.sched_getaffinity(0)))
+    P = wl.num_phys_pages
+
+    def run(n, nthreads, with_sets):
+        gomp.omp_set_num_threads(nthreads)
+        rows = np.linspace(0, wl.total_q - 1, n).astype(np.int32)
+        qr = attention_q_rows(wl, rows)
+        t0 = time.perf_counter()
+        sc = oracle.index_scores(wl.q_start, wl.hist_len, wl.q, "fp8", wl.q_scale, wl.kI, "fp8", wl.k_scale, wl.w,
+                                 rows)
+        t1 = time.perf_counter()
+        sel = oracle.topk(wl.q_start, wl.hist_len, rows, sc.astype(np.float32), wl.k)
+        t2 = time.perf_counter()
+        oracle.sparse_attn(wl.q_start, wl.hist_len, rows, qr, ai.k_pool, None, ai.k_row_stride, ai.v_row_stride,
+                           wl.page_table, wl.page_size, sel, ai.scale, ai.dv)
+        t3 = time.perf_counter()
+        stages = {"index_scores": (t1 - t0) / n, "topk": (t2 - t1) / n, "sparse_attn": (t3 - t2) / n}
+        sets = 0.0
+        if with_sets:
+            s0 = time.perf_counter()
+            bm, _, _ = oracle.page_demand(wl.q_start, wl.hist_len, gpu_sel, wl.page_table, wl.page_size, P)
+            oracle.runs(bm, P, wl.max_run)
+            oracle.predict_diff(bm, pred_bm, P, wl.max_run)
+            sets = time.perf_counter() - s0
+        return stages, sets, t3 - t0
+
+    stages, sets, dt = run(nrows, threads, True)
+    per_token = sum(stages.values()) + sets / wl.total_q
+    stages1, sets1, dt1 = run(nrows_1t, 1, True)
+    per_token1 = sum(stages1.values()) + sets1 / wl.total_q
+    gomp.omp_set_num_threads(threads)
+    return {"value": 1.0 / per_token, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{nrows} evenly spaced query rows of the same workload (scores over all ~139K candidates, "
+                      f"top-k, attention over k=2048; {dt:.1f} s) plus page demand, runs and the corrective set "
+                      f"over all 8192 rows' ids ({sets:.2f} s)",
+            "cpu_model": _cpu_model(), "nproc": os.cpu_count(), "cpus_allowed": len(os.sched_getaffinity(0)),
+            "seconds_per_token": stages, "set_stages_s": sets,
+            "single_thread": {"value": 1.0 / per_token1, "unit": "tokens/s", "cores": 1,
+                              "sample": f"{nrows_1t} evenly spaced rows ({dt1:.1f} s) plus the set stages over all "
+                                        f"rows ({sets1:.2f} s)", "seconds_per_token": stages1,
+                              "set_stages_s": sets1}}
 
 
 if __name__ == "__main__":

@@ -213,22 +213,32 @@ class Workload:
         return np.searchsorted(self.q_start, np.asarray(rows), side="right") - 1
 
 
-def _hot_spans(rng: np.random.Generator, M: int, n_spans: int = 8, frac: float = 0.05):
+def _hot_spans(rng: np.random.Generator, M: int, n_spans: int = 8, frac: float = 0.05, layout: str = "even"):
+    """frac of the M history tokens in n_spans equal spans, one placed
+    uniformly inside each of n_spans equal segments of the region: the whole
+    history ("even") or its most recent quarter ("recent")."""
     span = int(math.floor(frac * M / n_spans))
     spans = []
     if span <= 0:
         return spans
-    seg = M // n_spans
+    if layout == "even":
+        base, region = 0, M
+    elif layout == "recent":
+        base, region = M - M // 4, M // 4
+    else:
+        raise ValueError(layout)
+    seg = region // n_spans
     for j in range(n_spans):
-        lo = j * seg
+        lo = base + j * seg
         start = lo + int(rng.integers(0, max(seg - span, 0) + 1))
-        spans.append((start, span))
+        spans.append((start, min(span, M - start)))
     return spans
 
 
 def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_run=32,
                   seed=0, layer=0, w_scale=1.0, hot=True, table="identity",
-                  attn=None, q_pred_corr=None, name="custom", key_format=None, entry_shift=0) -> Workload:
+                  attn=None, q_pred_corr=None, name="custom", key_format=None, entry_shift=0,
+                  hot_frac=0.05, hot_layout="even") -> Workload:
     """Build one layer's indexer inputs for a (possibly ragged) batch of sessions.
 
     With ``entry_shift`` = e > 0 the keys, hot spans, pages and KV rows are
@@ -238,7 +248,10 @@ def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_ru
     ``table`` is "identity" (logical page p of session b -> physical page
     base_b + p) or "permuted" (one seeded permutation of the pool, sliced
     consecutively per session).  ``q_pred_corr`` = rho adds a predicted query
-    rho * q + sqrt(1 - rho^2) * N(0, 1), quantised on its own.
+    rho * q + sqrt(1 - rho^2) * N(0, 1), quantised on its own.  ``hot_frac``
+    and ``hot_layout`` set the share of history tokens in hot spans and where
+    the spans sit ("even": one in each eighth of the history; "recent": all
+    in its last quarter).
     """
     hist_len = np.asarray(hist_len, dtype=np.int32).reshape(-1)
     new_len = np.asarray(new_len, dtype=np.int32).reshape(-1)
@@ -252,7 +265,8 @@ def make_workload(*, hist_len, new_len, H, d, idx_dtype, k, page_size=64, max_ru
     # 1. hot spans (layer independent: the same positions in every layer)
     spans = []
     for b in range(B):
-        spans.append(_hot_spans(_rng(seed, S_HOT, b), int(hist_ids[b])) if hot else [])
+        spans.append(_hot_spans(_rng(seed, S_HOT, b), int(hist_ids[b]), frac=hot_frac, layout=hot_layout)
+                     if hot else [])
 
     # 2./3. indexer keys, history then new tokens, per session
     keys = []
