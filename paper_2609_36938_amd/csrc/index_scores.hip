@@ -454,6 +454,196 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     }
 }
 
+// bf16 queries and keys (d = 128, H = 64) on bf16 MFMA.  The structure of
+// the fp8 kernel above - 4 waves of 2 tokens, keys streamed through LDS in
+// 128-key stages by buffer-to-LDS DMA, XCD-aware key chunks, counted
+// buffer stores - with v_mfma_f32_16x16x32_bf16: a 16 (token, head) x 16
+// key tile takes four K-steps of 32 dims, and each key operand read from LDS
+// feeds the wave's 8 head tiles.  A key row is 256 bytes; its 16-byte chunk
+// c sits at slot c ^ (row & 15), so the 16 rows of one operand read fall in
+// 16 different bank groups.  The epilogue stays in fp32 (ReLU as a max, the
+// weighted head sum as fmas against fp32 weights): bf16 scores are held to
+// 1e-3 of the row maximum, which a bf16 rounding of each term would not
+// leave room for.
+constexpr int B16_ROW = 256;  // bytes per bf16 key row (128 dims)
+JANUS_DEV v8bf as_v8bf(v4i x) { return __builtin_bit_cast(v8bf, x); }
+
+__global__ __launch_bounds__(256, 2) void index_scores_bf16_mfma(
+    const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
+    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs, int es,
+    int nchunks, int key_chunk, int ntiles, const uint16_t *__restrict__ q, const float *__restrict__ q_scale,
+    const uint8_t *__restrict__ kI, const float *__restrict__ k_scale, const float *__restrict__ w,
+    float *__restrict__ scores)
+{
+    constexpr int H = 64, TPW = 2, RPT = 16 / TPW, HB = H / RPT, TOK_TILE = 4 * TPW;
+    __shared__ __attribute__((aligned(16))) uint8_t sKey0[IDX_STAGE * B16_ROW];
+    __shared__ __attribute__((aligned(16))) uint8_t sKey1[IDX_STAGE * B16_ROW];
+    __shared__ float sKs0[IDX_STAGE];
+    __shared__ float sKs1[IDX_STAGE];
+    int slot, chunk, b, tile0;
+    if (!xcd_tile_chunk(blockIdx.x, nchunks, ntiles, slot, chunk))
+        return;
+    if (!tile_slot(q_start, num_seqs, slot, TOK_TILE, b, tile0))
+        return;
+    const int N = q_start[b + 1] - q_start[b];
+    const int M = hist_len[b];
+    const int ctx = entries_of(M + N, es);
+    const int key_lo = chunk * key_chunk;
+    if (key_lo >= ctx)
+        return;
+    const int key_hi = min(ctx, key_lo + key_chunk);
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int tw0 = tile0 + wave * TPW;
+    const bool wave_on = tw0 < N;
+    const int r16 = lane & 15, kg = lane >> 4;
+    const int qrow0 = q_start[b];
+    const int64_t kbase = ctx_start[b];
+    const int block_lim = last_cand(M, min(tile0 + TOK_TILE - 1, N - 1), es);
+    const int key_end = min(key_hi, block_lim + 1);
+
+    // Key DMA: instruction j of wave `wave` fills stage bytes 4096j + 1024wave
+    // + 16lane = key row 16j + 4wave + lane/16, slot lane%16, which holds
+    // chunk (lane%16) ^ (row & 15); the lane's source offset is therefore
+    // fixed apart from 4096j.
+    const int drow = 4 * wave + (lane >> 4);
+    const uint32_t kvoff = (uint32_t)(B16_ROW * drow + 16 * ((lane & 15) ^ (drow & 15)));
+    auto issue = [&](int k0, uint8_t *kdst, float *sdst) {
+        const __amdgpu_buffer_rsrc_t krs =
+            make_buffer_rsrc((void *)(kI + (kbase + k0) * B16_ROW), (uint32_t)(ctx - k0) * B16_ROW);
+#pragma unroll
+        for (int j = 0; j < IDX_STAGE * B16_ROW / 16 / 256; ++j)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (lds_void_t *)(kdst + 4096 * j + 1024 * wave), 16,
+                                                     kvoff + 4096u * j, 0, 0, 0);
+        if (k_scale && wave < 2) {
+            const __amdgpu_buffer_rsrc_t srs =
+                make_buffer_rsrc((void *)(k_scale + kbase + k0), (uint32_t)(ctx - k0) << 2);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(srs, (lds_void_t *)(sdst + 64 * wave), 4, 4u * (64 * wave + lane),
+                                                     0, 0, 0);
+        }
+    };
+    if (key_lo < key_end)
+        issue(key_lo, sKey0, sKs0);
+
+    // A operand of head tile hb, K-step st: MFMA row r16 = (token r16/RPT,
+    // head RPT*hb + r16%RPT), dims 32st + 8kg .. +7
+    const int a_tok = tw0 + r16 / RPT;
+    const bool a_ok = a_tok < N;
+    const int64_t a_row = (int64_t)qrow0 + (a_ok ? a_tok : 0);
+    v8bf a[HB][4];
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+            a[hb][st] = a_ok ? as_v8bf(*(const v4i *)(q + (a_row * H + RPT * hb + (r16 % RPT)) * 128 + 32 * st + 8 * kg))
+                             : as_v8bf(v4i{0, 0, 0, 0});
+    // output rows 4kg..4kg+3 of every tile: token tw0 + 4kg/RPT, heads
+    // RPT*hb + (4kg)%RPT + i; their weights times the token's query scale
+    const int e_tok = tw0 + (4 * kg) / RPT;
+    const bool e_ok = e_tok < N;
+    const int64_t e_row = (int64_t)qrow0 + (e_ok ? e_tok : 0);
+    const int hsub = (4 * kg) % RPT;
+    const float sq = q_scale ? q_scale[e_row] : 1.0f;
+    float wv[HB][4];
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb) {
+        const v4f t = *(const v4f *)(w + e_row * H + RPT * hb + hsub);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            wv[hb][i] = t[i] * sq;
+    }
+    const int lim = last_cand(M, e_tok, es);
+    const int wave_lim = last_cand(M, min(tw0 + TPW - 1, N - 1), es);
+    constexpr int GPT = 4 / TPW;  // lane groups per token
+    const int gin = kg % GPT;
+    const int nrows_blk = max(0, min(TOK_TILE, N - tile0));
+    const int64_t blk_off = score_start[b] + (int64_t)tile0 * ctx;
+    const __amdgpu_buffer_rsrc_t rsrc = make_buffer_rsrc(scores + blk_off, (uint32_t)((int64_t)nrows_blk * ctx * 4));
+    const bool row_ok = e_ok && wave_on;
+    const uint32_t lane_row_off = (uint32_t)((int64_t)(e_tok - tile0) * ctx * 4);
+    constexpr int STORES_PER_GROUP = 4 / GPT;
+    constexpr int STAGE_STORES = (IDX_STAGE / 64) * STORES_PER_GROUP;
+    const int interior_end = min(ctx, last_cand(M, tile0, es) + 1);
+
+    auto stage = [&](int k0, const uint8_t *stg, const float *ks) {
+#pragma unroll
+        for (int gsub = 0; gsub < IDX_STAGE / 64; ++gsub) {
+            const int s0 = k0 + 64 * gsub;
+            if (s0 >= key_hi)
+                break;
+            float res[4];
+            const bool skip = !wave_on || s0 > wave_lim;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (skip) {
+                    res[j] = -INFINITY;
+                    continue;
+                }
+                // key operand of 16-key block (gsub, j): key row r = 64gsub +
+                // 16j + r16, chunk 4st + kg at slot (4st + kg) ^ r16
+                const uint8_t *rowb = stg + (64 * gsub + 16 * j + r16) * B16_ROW;
+                v8bf bk[4];
+#pragma unroll
+                for (int st = 0; st < 4; ++st)
+                    bk[st] = as_v8bf(*(const v4i *)(rowb + 16 * ((4 * st + kg) ^ r16)));
+                v4f d[HB];
+#pragma unroll
+                for (int hb = 0; hb < HB; ++hb)
+                    d[hb] = v4f{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int st = 0; st < 4; ++st)
+#pragma unroll
+                    for (int hb = 0; hb < HB; ++hb)
+                        d[hb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[hb][st], bk[st], d[hb], 0, 0, 0);
+                float r = 0.f;
+#pragma unroll
+                for (int hb = 0; hb < HB; ++hb)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i)
+                        r = fmaf(fmaxf(d[hb][i], 0.f), wv[hb][i], r);
+                r += xor_lanes16(r);  // the other lane group of this token (GPT = 2)
+                res[j] = r;
+            }
+#pragma unroll
+            for (int js = 0; js < STORES_PER_GROUP; ++js) {
+                float v = res[js * GPT];
+#pragma unroll
+                for (int u = 1; u < GPT; ++u)
+                    v = gin == u ? res[js * GPT + u] : v;
+                const int jj = js * GPT + gin;
+                const int s = s0 + 16 * jj + r16;
+                const float kscale = k_scale ? ks[64 * gsub + 16 * jj + r16] : 1.0f;
+                uint32_t off;
+                if (s0 + 64 <= interior_end) {
+                    v *= kscale;
+                    off = row_ok ? lane_row_off + 4u * (uint32_t)s : 0x80000000u;
+                } else {
+                    v = s > lim ? -INFINITY : v * kscale;
+                    off = (row_ok && s < ctx) ? lane_row_off + 4u * (uint32_t)s : 0x80000000u;
+                }
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rsrc, off, 0, 0);
+            }
+        }
+    };
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int k0 = key_lo; k0 < key_hi; k0 += 2 * IDX_STAGE) {
+        if (k0 + IDX_STAGE < key_end)
+            issue(k0 + IDX_STAGE, sKey1, sKs1);
+        __builtin_amdgcn_sched_barrier(0);
+        stage(k0, sKey0, sKs0);
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(STAGE_STORES));
+        lds_barrier();
+        if (k0 + IDX_STAGE >= key_hi)
+            break;
+        if (k0 + 2 * IDX_STAGE < key_end)
+            issue(k0 + 2 * IDX_STAGE, sKey0, sKs0);
+        __builtin_amdgcn_sched_barrier(0);
+        stage(k0 + IDX_STAGE, sKey1, sKs1);
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(STAGE_STORES));
+        lds_barrier();
+    }
+}
+
 // Plain vector kernel for any dtype and shape: one (token, key) score per thread.
 __global__ __launch_bounds__(256) void index_scores_vector(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
@@ -769,6 +959,20 @@ extern "C" int janus_index_scores(const janus_batch *bt, const void *q, janus_dt
         hipLaunchKernelGGL((index_scores_fp8_mfma<64, TPW>), dim3(IDX_XCD * per_xcd), dim3(256), 0, st, bt->q_start,
                            bt->ctx_start, bt->hist_len, bt->score_start, nseq, bt->entry_shift, nchunks, key_chunk, ntiles,
                            (const uint8_t *)q, q_scale, (const uint8_t *)kI, k_scale, w, scores);
+        return launch_status();
+    }
+    if (q_dt == JANUS_BF16 && d == 128 && H == 64 && bt->max_ctx <= (1 << 23)) {
+        // bf16 on bf16 MFMA: the fp8 kernel's key chunking (32-bit buffer
+        // offsets over 256-byte key rows: contexts up to 2^23)
+        const int per_xcd_keys = ceil_div(bt->max_ctx, IDX_XCD);
+        const int chunks_per_xcd = std::max(1, ceil_div(per_xcd_keys, IDX_KEY_CHUNK));
+        const int key_chunk = ceil_div(ceil_div(per_xcd_keys, chunks_per_xcd), IDX_STAGE) * IDX_STAGE;
+        const int nchunks = ceil_div(bt->max_ctx, key_chunk);
+        const int ntiles = ceil_div(bt->total_q, 8) + nseq;
+        const int per_xcd = ceil_div(nchunks, IDX_XCD) * ntiles;
+        hipLaunchKernelGGL(index_scores_bf16_mfma, dim3(IDX_XCD * per_xcd), dim3(256), 0, st, bt->q_start,
+                           bt->ctx_start, bt->hist_len, bt->score_start, nseq, bt->entry_shift, nchunks, key_chunk,
+                           ntiles, (const uint16_t *)q, q_scale, (const uint8_t *)kI, k_scale, w, scores);
         return launch_status();
     }
     dim3 grid(ceil_div(bt->max_ctx, GEN_KEY_TILE), ceil_div(bt->total_q, GEN_TOK_TILE) + nseq);
