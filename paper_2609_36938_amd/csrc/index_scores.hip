@@ -644,6 +644,195 @@ __global__ __launch_bounds__(256, 2) void index_scores_bf16_mfma(
     }
 }
 
+// MXFP4 keys at prefill: the fp8 kernel's structure with the fp8 x fp4
+// scaled MFMA consuming the keys as stored.  For an fp4 operand the MFMA takes
+// 16 contiguous bytes per lane: lane group g holds elements 32g .. 32g+31
+// (element j in the low nibble of byte j/2 when j is even), which is exactly
+// MX block g of a key, and it applies the E8M0 scale that lane group g
+// supplies to that block - so each lane passes its key's scale for block g.
+// The fp8 query operand keeps its own layout (dims 16g .. 16g+15 in
+// registers 0-3, 64+16g .. in 4-7).  Key rows are 64 bytes in LDS, chunk c
+// of row r at slot c ^ ((r >> 2) & 3), so the 16 rows of an operand read
+// fall in 16 different bank groups.  Block scales make a product of any size,
+// so the epilogue rounds each pair to bf16, clamps its sign with a packed
+// int16 max and dots it with the bf16 weights (relative error <= 2^-8 per
+// term), as the row-tile MXFP4 path does.
+constexpr int F4_ROW = 64;  // bytes of e2m1 codes per key (128 dims)
+
+__global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
+    const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
+    const int32_t *__restrict__ hist_len, const int64_t *__restrict__ score_start, int num_seqs, int es,
+    int nchunks, int key_chunk, int ntiles, const uint8_t *__restrict__ q, const float *__restrict__ q_scale,
+    const uint8_t *__restrict__ kI, const uint8_t *__restrict__ k_bscale, const float *__restrict__ k_scale,
+    const float *__restrict__ w, float *__restrict__ scores)
+{
+    constexpr int H = 64, TPW = 2, RPT = 16 / TPW, HB = H / RPT, TOK_TILE = 4 * TPW;
+    __shared__ __attribute__((aligned(16))) uint8_t sKey0[IDX_STAGE * F4_ROW];
+    __shared__ __attribute__((aligned(16))) uint8_t sKey1[IDX_STAGE * F4_ROW];
+    __shared__ uint32_t sBs0[IDX_STAGE];  // the 4 E8M0 block scales of each key
+    __shared__ uint32_t sBs1[IDX_STAGE];
+    __shared__ float sKs0[IDX_STAGE];
+    __shared__ float sKs1[IDX_STAGE];
+    int slot, chunk, b, tile0;
+    if (!xcd_tile_chunk(blockIdx.x, nchunks, ntiles, slot, chunk))
+        return;
+    if (!tile_slot(q_start, num_seqs, slot, TOK_TILE, b, tile0))
+        return;
+    const int N = q_start[b + 1] - q_start[b];
+    const int M = hist_len[b];
+    const int ctx = entries_of(M + N, es);
+    const int key_lo = chunk * key_chunk;
+    if (key_lo >= ctx)
+        return;
+    const int key_hi = min(ctx, key_lo + key_chunk);
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int tw0 = tile0 + wave * TPW;
+    const bool wave_on = tw0 < N;
+    const int r16 = lane & 15, kg = lane >> 4;
+    const int qrow0 = q_start[b];
+    const int64_t kbase = ctx_start[b];
+    const int block_lim = last_cand(M, min(tile0 + TOK_TILE - 1, N - 1), es);
+    const int key_end = min(key_hi, block_lim + 1);
+
+    // Key DMA: instruction i of wave `wave` fills stage bytes 4096i + 1024wave
+    // + 16lane = key row 64i + 16wave + lane/4, slot lane%4, which holds chunk
+    // (lane%4) ^ ((lane/16) & 3); block scales by waves 2 and 3, key scales
+    // by waves 0 and 1 (one dword per lane)
+    const uint32_t kvoff = 1024u * wave + 64u * (lane >> 2) + 16u * ((lane & 3) ^ ((lane >> 4) & 3));
+    auto issue = [&](int k0, uint8_t *kdst, uint32_t *bdst, float *sdst) {
+        const __amdgpu_buffer_rsrc_t krs =
+            make_buffer_rsrc((void *)(kI + (kbase + k0) * F4_ROW), (uint32_t)(ctx - k0) * F4_ROW);
+#pragma unroll
+        for (int i = 0; i < IDX_STAGE * F4_ROW / 16 / 256; ++i)
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (lds_void_t *)(kdst + 4096 * i + 1024 * wave), 16,
+                                                     kvoff + 4096u * i, 0, 0, 0);
+        if (wave >= 2) {
+            const __amdgpu_buffer_rsrc_t brs =
+                make_buffer_rsrc((void *)(k_bscale + (kbase + k0) * 4), (uint32_t)(ctx - k0) << 2);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(brs, (lds_void_t *)(bdst + 64 * (wave - 2)), 4,
+                                                     4u * (64 * (wave - 2) + lane), 0, 0, 0);
+        } else if (k_scale) {
+            const __amdgpu_buffer_rsrc_t srs =
+                make_buffer_rsrc((void *)(k_scale + kbase + k0), (uint32_t)(ctx - k0) << 2);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(srs, (lds_void_t *)(sdst + 64 * wave), 4, 4u * (64 * wave + lane),
+                                                     0, 0, 0);
+        }
+    };
+    if (key_lo < key_end)
+        issue(key_lo, sKey0, sBs0, sKs0);
+
+    // A operand of head tile hb: row r16 = (token r16/RPT, head RPT*hb +
+    // r16%RPT); registers 0-3 = query bytes 16kg .., 4-7 = bytes 64+16kg ..
+    const int a_tok = tw0 + r16 / RPT;
+    const bool a_ok = a_tok < N;
+    const int64_t a_row = (int64_t)qrow0 + (a_ok ? a_tok : 0);
+    v8i a[HB];
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb) {
+        const uint8_t *qr = q + ((a_row * H + RPT * hb + (r16 % RPT)) << 7);
+        const v4i lo = a_ok ? *(const v4i *)(qr + 16 * kg) : v4i{0, 0, 0, 0};
+        const v4i hi = a_ok ? *(const v4i *)(qr + 64 + 16 * kg) : v4i{0, 0, 0, 0};
+        a[hb] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    }
+    // output rows 4kg..4kg+3 of every tile: token tw0 + 4kg/RPT, heads
+    // RPT*hb + (4kg)%RPT + i; bf16 weights times the token's query scale
+    const int e_tok = tw0 + (4 * kg) / RPT;
+    const bool e_ok = e_tok < N;
+    const int64_t e_row = (int64_t)qrow0 + (e_ok ? e_tok : 0);
+    const int hsub = (4 * kg) % RPT;
+    const float sq = q_scale ? q_scale[e_row] : 1.0f;
+    v2bf wv[HB][2];
+#pragma unroll
+    for (int hb = 0; hb < HB; ++hb) {
+        const v4f t = *(const v4f *)(w + e_row * H + RPT * hb + hsub);
+        wv[hb][0] = __builtin_convertvector((v2f){t[0] * sq, t[1] * sq}, v2bf);
+        wv[hb][1] = __builtin_convertvector((v2f){t[2] * sq, t[3] * sq}, v2bf);
+    }
+    const int lim = last_cand(M, e_tok, es);
+    const int wave_lim = last_cand(M, min(tw0 + TPW - 1, N - 1), es);
+    constexpr int GPT = 4 / TPW;
+    const int gin = kg % GPT;
+    const int nrows_blk = max(0, min(TOK_TILE, N - tile0));
+    const int64_t blk_off = score_start[b] + (int64_t)tile0 * ctx;
+    const __amdgpu_buffer_rsrc_t rsrc = make_buffer_rsrc(scores + blk_off, (uint32_t)((int64_t)nrows_blk * ctx * 4));
+    const bool row_ok = e_ok && wave_on;
+    const uint32_t lane_row_off = (uint32_t)((int64_t)(e_tok - tile0) * ctx * 4);
+    constexpr int STORES_PER_GROUP = 4 / GPT;
+    constexpr int STAGE_STORES = (IDX_STAGE / 64) * STORES_PER_GROUP;
+    const int interior_end = min(ctx, last_cand(M, tile0, es) + 1);
+    // this lane's B chunk (key row r16 of a 16-key block, bytes 16kg ..)
+    const int boff = r16 * F4_ROW + 16 * (kg ^ ((r16 >> 2) & 3));
+
+    auto stage = [&](int k0, const uint8_t *stg, const uint32_t *bs, const float *ks) {
+#pragma unroll
+        for (int gsub = 0; gsub < IDX_STAGE / 64; ++gsub) {
+            const int s0 = k0 + 64 * gsub;
+            if (s0 >= key_hi)
+                break;
+            float res[4];
+            const bool skip = !wave_on || s0 > wave_lim;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (skip) {
+                    res[j] = -INFINITY;
+                    continue;
+                }
+                const int row = 64 * gsub + 16 * j;  // first key of the 16-key block
+                const v4i kb4 = *(const v4i *)(stg + row * F4_ROW + boff);
+                const v8i bk = v8i{kb4[0], kb4[1], kb4[2], kb4[3], 0, 0, 0, 0};
+                const int sb = (int)((bs[row + r16] >> (8 * kg)) & 0xFFu);  // E8M0 of block kg
+                float r = 0.f;
+#pragma unroll
+                for (int hb = 0; hb < HB; ++hb) {
+                    const v4f d = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a[hb], bk, v4f{0.f, 0.f, 0.f, 0.f},
+                                                                                  0, 4, 0, 127, 0, sb);
+                    r = __builtin_amdgcn_fdot2_f32_bf16(relu_bf16x2(d[0], d[1]), wv[hb][0], r, false);
+                    r = __builtin_amdgcn_fdot2_f32_bf16(relu_bf16x2(d[2], d[3]), wv[hb][1], r, false);
+                }
+                r += xor_lanes16(r);
+                res[j] = r;
+            }
+#pragma unroll
+            for (int js = 0; js < STORES_PER_GROUP; ++js) {
+                float v = res[js * GPT];
+#pragma unroll
+                for (int u = 1; u < GPT; ++u)
+                    v = gin == u ? res[js * GPT + u] : v;
+                const int jj = js * GPT + gin;
+                const int s = s0 + 16 * jj + r16;
+                const float kscale = k_scale ? ks[64 * gsub + 16 * jj + r16] : 1.0f;
+                uint32_t off;
+                if (s0 + 64 <= interior_end) {
+                    v *= kscale;
+                    off = row_ok ? lane_row_off + 4u * (uint32_t)s : 0x80000000u;
+                } else {
+                    v = s > lim ? -INFINITY : v * kscale;
+                    off = (row_ok && s < ctx) ? lane_row_off + 4u * (uint32_t)s : 0x80000000u;
+                }
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rsrc, off, 0, 0);
+            }
+        }
+    };
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    for (int k0 = key_lo; k0 < key_hi; k0 += 2 * IDX_STAGE) {
+        if (k0 + IDX_STAGE < key_end)
+            issue(k0 + IDX_STAGE, sKey1, sBs1, sKs1);
+        __builtin_amdgcn_sched_barrier(0);
+        stage(k0, sKey0, sBs0, sKs0);
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(STAGE_STORES));
+        lds_barrier();
+        if (k0 + IDX_STAGE >= key_hi)
+            break;
+        if (k0 + 2 * IDX_STAGE < key_end)
+            issue(k0 + 2 * IDX_STAGE, sKey0, sBs0, sKs0);
+        __builtin_amdgcn_sched_barrier(0);
+        stage(k0 + IDX_STAGE, sKey1, sBs1, sKs1);
+        __builtin_amdgcn_s_waitcnt(vmcnt_only(STAGE_STORES));
+        lds_barrier();
+    }
+}
+
 // Plain vector kernel for any dtype and shape: one (token, key) score per thread.
 __global__ __launch_bounds__(256) void index_scores_vector(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
@@ -994,6 +1183,21 @@ extern "C" int janus_index_scores_mxfp4(const janus_batch *bt, const void *q, co
         return JANUS_ERR_UNSUPPORTED;
     if (bt->total_q == 0 || bt->max_ctx == 0)
         return JANUS_OK;
-    launch_rows<true>(bt, q, q_scale, kI, k_block_scale, k_scale, w, scores, as_stream(stream));
+    if (bt->max_q <= ROWS_NQ) {
+        // decode-shaped: the row-tile kernel
+        launch_rows<true>(bt, q, q_scale, kI, k_block_scale, k_scale, w, scores, as_stream(stream));
+        return launch_status();
+    }
+    // prefill-shaped: keys staged through LDS, the fp8 kernel's chunking
+    const int per_xcd_keys = ceil_div(bt->max_ctx, IDX_XCD);
+    const int chunks_per_xcd = std::max(1, ceil_div(per_xcd_keys, IDX_KEY_CHUNK));
+    const int key_chunk = ceil_div(ceil_div(per_xcd_keys, chunks_per_xcd), IDX_STAGE) * IDX_STAGE;
+    const int nchunks = ceil_div(bt->max_ctx, key_chunk);
+    const int ntiles = ceil_div(bt->total_q, 8) + bt->num_seqs;
+    const int per_xcd = ceil_div(nchunks, IDX_XCD) * ntiles;
+    hipLaunchKernelGGL(index_scores_mxfp4_mfma, dim3(IDX_XCD * per_xcd), dim3(256), 0, as_stream(stream),
+                       bt->q_start, bt->ctx_start, bt->hist_len, bt->score_start, bt->num_seqs, bt->entry_shift,
+                       nchunks, key_chunk, ntiles, (const uint8_t *)q, q_scale, (const uint8_t *)kI, k_block_scale,
+                       k_scale, w, scores);
     return launch_status();
 }
