@@ -171,6 +171,8 @@ def main():
     counts = diff_out[2].cpu().tolist()
     extras = not args.core_only
     spread = spread_attention(janus, torch, wl, bt, qa, kv, pt, ai, max(args.steps, 5)) if extras else None
+    mxfp4 = mxfp4_prefill(janus, torch, bt, scores, max(args.steps, 5), per["index_scores"], idx_flop) \
+        if extras else None
     sweep = prediction_sweep(janus, torch, max(args.steps, 5)) if extras else None
     predicted = predicted_path(janus, torch, args.c4_layers) if extras and args.c4_layers > 0 else None
     decode = decode_step(janus, torch, max(args.steps, 5)) if extras and not args.no_decode else None
@@ -211,6 +213,7 @@ def main():
         },
         "demand": {"pages": int(pd_out[3][0]), "runs": int(pd_out[3][1]), "pred_counts": counts},
         "sparse_attn_spread": spread,
+        "mxfp4_prefill": mxfp4,
         "prediction_sweep": sweep,
         "predicted_path": predicted,
         "decode": decode,
@@ -310,6 +313,34 @@ def spread_attention(janus, torch, wl, bt, qa, kv, pt, ai, steps):
                         "range (the whole 160 MB pool is gathered)",
             "ms": ms, "gather_GBps_logical": gather / (ms * 1e-3) / 1e9,
             "gather_frac_hbm": gather / (ms * 1e-3) / PEAK_HBM}
+
+
+def mxfp4_prefill(janus, torch, bt, scores, steps, fp8_ms, flop):
+    """The indexer of the 128K workload with its keys in MXFP4 (DeepSeek-V4
+    keeps indexer keys in FP4, Sec. 5.1): the same draws quantised to e2m1
+    codes with one E8M0 scale per 32 elements, fp8 queries; times the
+    prefill kernel against the fp8-key indexer of the step."""
+    from workloads import make_workload
+    wl = make_workload(hist_len=[131072], new_len=[8192], H=64, d=128, idx_dtype="fp8", k=2048, seed=2,
+                       w_scale=1.0 / 8, key_format="mxfp4")
+    dev = scores.device
+    T = lambda a: torch.from_numpy(np.ascontiguousarray(a)).to(dev)
+    q, kI, bs, w, sq = T(wl.q), T(wl.kI), T(wl.k_bscale), T(wl.w), T(wl.q_scale)
+    f = lambda: janus.index_scores_mxfp4(bt, q, kI, bs, w, q_scale=sq, scores=scores)
+    f()
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(steps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        f()
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = float(np.median(ts))
+    return {"workload": "index scores of the 128K workload with MXFP4 keys (64 B of e2m1 + 4 E8M0 scales per key)",
+            "ms": ms, "TFLOPs": flop / ms / 1e9, "frac_fp8_peak": flop / (ms * 1e-3) / PEAK_FP8,
+            "fp8_keys_ms": fp8_ms, "ratio_to_fp8_keys": ms / fp8_ms}
 
 
 SWEEP_LAYOUTS = (("hot spans 1% of the history (fewer tokens than k), one in each eighth", 0.01, "even"),
