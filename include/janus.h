@@ -149,8 +149,13 @@ int janus_index_scores(const janus_batch *b,
  *   w, scores      as for janus_index_scores
  * Products run on the fp8 x fp4 block-scaled MFMA; each head's product is
  * rounded to bf16 and the head weights are applied in bf16 (relative error
- * <= 2^-8 per term).  Requires H = 64, d = 128 and contexts up to 2^24 tokens
- * (else JANUS_ERR_UNSUPPORTED; d not a multiple of 32: JANUS_ERR_INVALID_ARG).
+ * <= 2^-8 per term).  For batches with more than 4 appended tokens in a
+ * session, each key's block scales are taken relative to the largest of its
+ * d/32 (exact), except that a block more than 2^127 below that largest one
+ * counts as exactly 2^-127 of it.  The E8M0 code 255 (NaN) is not a
+ * supported input: such a key's scores are unspecified.  Requires H = 64,
+ * d = 128 and contexts up to 2^24 tokens (else JANUS_ERR_UNSUPPORTED; d not a
+ * multiple of 32: JANUS_ERR_INVALID_ARG).
  */
 int janus_index_scores_mxfp4(const janus_batch *b,
                              const void *q, const float *q_scale,

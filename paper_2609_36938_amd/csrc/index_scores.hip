@@ -157,6 +157,59 @@ JANUS_DEV void head_group(float &acc, const v8i &a0, const v8i &a1, const v8i &a
         [w00] "v"(w[0][0]), [w01] "v"(w[0][1]), [w10] "v"(w[1][0]), [w11] "v"(w[1][1]), [w20] "v"(w[2][0]), \
         [w21] "v"(w[2][1]), [w30] "v"(w[3][0]), [w31] "v"(w[3][1])
 
+// The fp8 group above with e2m1 keys as the B operand (blgp 4: 16 bytes per
+// lane, lane group g holding the key's elements 32g .. 32g+31, MX block g)
+// and separate scales: sa = 2^-25 for the queries, sb = the lane's block
+// scale divided by the largest of its key's four (so at most 1).  Every
+// product then stays below 128 * 448 * 6 * 2^-25 < 1 in magnitude and the
+// clamping convert is ReLU, as in the fp8 group; the wait states are the fp8
+// group's (the same 8-pass MFMA), with one more after the fourth MFMA.
+#define IDX_MFMA_F4C(dst, a) \
+    "v_mfma_scale_f32_16x16x128_f8f6f4 " dst ", %[" a "], %[bk], 0, %[sa], %[sb] op_sel_hi:[0,0,0] blgp:4\n\t"
+#define IDX_HEAD_GROUP_F4C(INIT)                                                                     \
+    INIT "s_nop 1\n\t" IDX_MFMA_F4C("v[112:115]", "a0") IDX_MFMA_F4C("v[116:119]", "a1")            \
+        IDX_MFMA_F4C("v[120:123]", "a2") IDX_MFMA_F4C("v[124:127]", "a3")                          \
+    "s_nop 1\n\t"                                                                                     \
+    "v_cvt_pk_bf16_f32 v112, v112, v113 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v114, v114, v115 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v112, %[w00]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v116, v116, v117 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v114, %[w01]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v118, v118, v119 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v116, %[w10]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v120, v120, v121 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v118, %[w11]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v122, v122, v123 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v120, %[w20]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v124, v124, v125 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v122, %[w21]\n\t"                                                       \
+    "v_cvt_pk_bf16_f32 v126, v126, v127 clamp\n\t"                                                    \
+    "v_dot2c_f32_bf16 %[acc], v124, %[w30]\n\t"                                                       \
+    "s_nop 0\n\t"                                                                                     \
+    "v_dot2c_f32_bf16 %[acc], v126, %[w31]\n\t"                                                       \
+    "s_nop 2"
+#define IDX_HEAD_GROUP_F4C_INPUTS                                                                      \
+    [a0] "v"(a0), [a1] "v"(a1), [a2] "v"(a2), [a3] "v"(a3), [bk] "v"(bk), [sa] "v"(sa), [sb] "v"(sb),   \
+        [w00] "v"(w[0][0]), [w01] "v"(w[0][1]), [w10] "v"(w[1][0]), [w11] "v"(w[1][1]), [w20] "v"(w[2][0]), \
+        [w21] "v"(w[2][1]), [w30] "v"(w[3][0]), [w31] "v"(w[3][1])
+
+template <bool FIRST>
+JANUS_DEV void head_group_f4c(float &acc, const v8i &a0, const v8i &a1, const v8i &a2, const v8i &a3, const v4i &bk,
+                              int sa, int sb, const v2bf (*w)[2])
+{
+    if (FIRST)
+        asm(IDX_HEAD_GROUP_F4C("v_mov_b32 %[acc], 0\n\t")
+            : [acc] "=&v"(acc)
+            : IDX_HEAD_GROUP_F4C_INPUTS
+            : IDX_HEAD_GROUP_CLOBBERS);
+    else
+        asm(IDX_HEAD_GROUP_F4C("")
+            : [acc] "+v"(acc)
+            : IDX_HEAD_GROUP_F4C_INPUTS
+            : IDX_HEAD_GROUP_CLOBBERS);
+}
+constexpr int IDX_SCALE_2M25 = 127 - 25;  // E8M0 2^-25
+
 // MXFP4 keys as fp8: an e2m1 nibble (sign, 2-bit exponent, 1-bit mantissa,
 // bias 1) placed at bits 7 and 4..2 of a byte is the e4m3 code (bias 7) of
 // the same value times 2^-6; the e2m1 subnormal 0.5 lands on the e4m3
@@ -213,6 +266,8 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 
 // s_waitcnt immediate (gfx9 encoding) that waits for vmcnt <= n only.
 constexpr int vmcnt_only(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+// s_waitcnt immediate that waits for lgkmcnt = 0 only.
+constexpr int IDX_LGKM0 = 15 | (3 << 14) | (7 << 4);
 
 // Wave-uniform buffer resource over [base, base + bytes): stores past
 // `bytes` are dropped by the hardware.
@@ -653,10 +708,13 @@ __global__ __launch_bounds__(256, 2) void index_scores_bf16_mfma(
 // The fp8 query operand keeps its own layout (dims 16g .. 16g+15 in
 // registers 0-3, 64+16g .. in 4-7).  Key rows are 64 bytes in LDS, chunk c
 // of row r at slot c ^ ((r >> 2) & 3), so the 16 rows of an operand read
-// fall in 16 different bank groups.  Block scales make a product of any size,
-// so the epilogue rounds each pair to bf16, clamps its sign with a packed
-// int16 max and dots it with the bf16 weights (relative error <= 2^-8 per
-// term), as the row-tile MXFP4 path does.
+// fall in 16 different bank groups.  Each key's block scales are divided by
+// the largest of the four (E8M0 exponents minus the largest, clamped at
+// 2^-127) and its key scale multiplied by that largest one, once per stage by
+// the two waves that load them: with the query scale 2^-25 every product is
+// then below 1 in magnitude and the epilogue is the fp8 kernel's clamping
+// convert and dot product (4 VALU per MFMA).  Dividing by a power of two
+// changes no rounding, so the scores are those of the unnormalised products.
 constexpr int F4_ROW = 64;  // bytes of e2m1 codes per key (128 dims)
 
 __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
@@ -696,8 +754,8 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
 
     // Key DMA: instruction i of wave `wave` fills stage bytes 4096i + 1024wave
     // + 16lane = key row 64i + 16wave + lane/4, slot lane%4, which holds chunk
-    // (lane%4) ^ ((lane/16) & 3); block scales by waves 2 and 3, key scales
-    // by waves 0 and 1 (one dword per lane)
+    // (lane%4) ^ ((lane/16) & 3); waves 2 and 3 also load the block scales and
+    // key scales of keys 64(wave-2) .. +63 (one dword per lane each)
     const uint32_t kvoff = 1024u * wave + 64u * (lane >> 2) + 16u * ((lane & 3) ^ ((lane >> 4) & 3));
     auto issue = [&](int k0, uint8_t *kdst, uint32_t *bdst, float *sdst) {
         const __amdgpu_buffer_rsrc_t krs =
@@ -711,12 +769,30 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
                 make_buffer_rsrc((void *)(k_bscale + (kbase + k0) * 4), (uint32_t)(ctx - k0) << 2);
             __builtin_amdgcn_raw_ptr_buffer_load_lds(brs, (lds_void_t *)(bdst + 64 * (wave - 2)), 4,
                                                      4u * (64 * (wave - 2) + lane), 0, 0, 0);
-        } else if (k_scale) {
-            const __amdgpu_buffer_rsrc_t srs =
-                make_buffer_rsrc((void *)(k_scale + kbase + k0), (uint32_t)(ctx - k0) << 2);
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(srs, (lds_void_t *)(sdst + 64 * wave), 4, 4u * (64 * wave + lane),
-                                                     0, 0, 0);
+            if (k_scale) {
+                const __amdgpu_buffer_rsrc_t srs =
+                    make_buffer_rsrc((void *)(k_scale + kbase + k0), (uint32_t)(ctx - k0) << 2);
+                __builtin_amdgcn_raw_ptr_buffer_load_lds(srs, (lds_void_t *)(sdst + 64 * (wave - 2)), 4,
+                                                         4u * (64 * (wave - 2) + lane), 0, 0, 0);
+            }
         }
+    };
+    // Normalise the block scales of this wave's 64 keys in a stage whose
+    // loads have landed (waves 2 and 3): exponents minus the key's largest
+    // (at least 0), and the key scale times 2^(largest - 127).  The LDS writes
+    // complete before the wave moves on.
+    auto normalise = [&](uint32_t *bsb, float *ksb) {
+        const int key = 64 * (wave - 2) + lane;
+        const uint32_t e = bsb[key];
+        const int e0 = (int)(e & 0xFFu), e1 = (int)((e >> 8) & 0xFFu), e2 = (int)((e >> 16) & 0xFFu),
+                  e3 = (int)(e >> 24);
+        const int em = max(max(e0, e1), max(e2, e3));
+        const uint32_t n0 = (uint32_t)max(e0 + 127 - em, 0), n1 = (uint32_t)max(e1 + 127 - em, 0),
+                       n2 = (uint32_t)max(e2 + 127 - em, 0), n3 = (uint32_t)max(e3 + 127 - em, 0);
+        const float ks = k_scale ? ksb[key] : 1.0f;
+        bsb[key] = n0 | (n1 << 8) | (n2 << 16) | (n3 << 24);
+        ksb[key] = ks * __builtin_ldexpf(1.0f, em - 127);
+        __builtin_amdgcn_s_waitcnt(IDX_LGKM0);
     };
     if (key_lo < key_end)
         issue(key_lo, sKey0, sBs0, sKs0);
@@ -740,7 +816,9 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
     const bool e_ok = e_tok < N;
     const int64_t e_row = (int64_t)qrow0 + (e_ok ? e_tok : 0);
     const int hsub = (4 * kg) % RPT;
-    const float sq = q_scale ? q_scale[e_row] : 1.0f;
+    // head weights times the token's query scale and 2^25 (undoing the
+    // MFMA's query scale), rounded once to bf16 pairs
+    const float sq = (q_scale ? q_scale[e_row] : 1.0f) * 0x1p25f;
     v2bf wv[HB][2];
 #pragma unroll
     for (int hb = 0; hb < HB; ++hb) {
@@ -748,6 +826,7 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
         wv[hb][0] = __builtin_convertvector((v2f){t[0] * sq, t[1] * sq}, v2bf);
         wv[hb][1] = __builtin_convertvector((v2f){t[2] * sq, t[3] * sq}, v2bf);
     }
+    const int sa = IDX_SCALE_2M25;
     const int lim = last_cand(M, e_tok, es);
     const int wave_lim = last_cand(M, min(tw0 + TPW - 1, N - 1), es);
     constexpr int GPT = 4 / TPW;
@@ -763,7 +842,11 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
     // this lane's B chunk (key row r16 of a 16-key block, bytes 16kg ..)
     const int boff = r16 * F4_ROW + 16 * (kg ^ ((r16 >> 2) & 3));
 
-    auto stage = [&](int k0, const uint8_t *stg, const uint32_t *bs, const float *ks) {
+    // one stage: compute the keys in (stg, bs, ks); waves 2 and 3 normalise
+    // the next stage's scales (nbs, nks) half way through, once its loads
+    // (issued before this stage's stores) have landed
+    auto stage = [&](int k0, const uint8_t *stg, const uint32_t *bs, const float *ks, uint32_t *nbs, float *nks,
+                     bool next) {
 #pragma unroll
         for (int gsub = 0; gsub < IDX_STAGE / 64; ++gsub) {
             const int s0 = k0 + 64 * gsub;
@@ -778,17 +861,11 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
                     continue;
                 }
                 const int row = 64 * gsub + 16 * j;  // first key of the 16-key block
-                const v4i kb4 = *(const v4i *)(stg + row * F4_ROW + boff);
-                const v8i bk = v8i{kb4[0], kb4[1], kb4[2], kb4[3], 0, 0, 0, 0};
-                const int sb = (int)((bs[row + r16] >> (8 * kg)) & 0xFFu);  // E8M0 of block kg
-                float r = 0.f;
-#pragma unroll
-                for (int hb = 0; hb < HB; ++hb) {
-                    const v4f d = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a[hb], bk, v4f{0.f, 0.f, 0.f, 0.f},
-                                                                                  0, 4, 0, 127, 0, sb);
-                    r = __builtin_amdgcn_fdot2_f32_bf16(relu_bf16x2(d[0], d[1]), wv[hb][0], r, false);
-                    r = __builtin_amdgcn_fdot2_f32_bf16(relu_bf16x2(d[2], d[3]), wv[hb][1], r, false);
-                }
+                const v4i bk = *(const v4i *)(stg + row * F4_ROW + boff);
+                const int sb = (int)((bs[row + r16] >> (8 * kg)) & 0xFFu);  // normalised E8M0 of block kg
+                float r;
+                head_group_f4c<true>(r, a[0], a[1], a[2], a[3], bk, sa, sb, &wv[0]);
+                head_group_f4c<false>(r, a[4], a[5], a[6], a[7], bk, sa, sb, &wv[4]);
                 r += xor_lanes16(r);
                 res[j] = r;
             }
@@ -800,7 +877,7 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
                     v = gin == u ? res[js * GPT + u] : v;
                 const int jj = js * GPT + gin;
                 const int s = s0 + 16 * jj + r16;
-                const float kscale = k_scale ? ks[64 * gsub + 16 * jj + r16] : 1.0f;
+                const float kscale = ks[64 * gsub + 16 * jj + r16];
                 uint32_t off;
                 if (s0 + 64 <= interior_end) {
                     v *= kscale;
@@ -811,23 +888,34 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
                 }
                 __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rsrc, off, 0, 0);
             }
+            if (gsub == 0 && next && wave >= 2) {
+                // the next stage's loads precede this group's stores
+                __builtin_amdgcn_sched_barrier(0);
+                __builtin_amdgcn_s_waitcnt(vmcnt_only(STORES_PER_GROUP));
+                normalise(nbs, nks);
+                __builtin_amdgcn_sched_barrier(0);
+            }
         }
     };
     __builtin_amdgcn_s_waitcnt(0);
+    if (key_lo < key_end && wave >= 2)
+        normalise(sBs0, sKs0);
     __syncthreads();
     for (int k0 = key_lo; k0 < key_hi; k0 += 2 * IDX_STAGE) {
-        if (k0 + IDX_STAGE < key_end)
+        const bool n1 = k0 + IDX_STAGE < key_end;
+        if (n1)
             issue(k0 + IDX_STAGE, sKey1, sBs1, sKs1);
         __builtin_amdgcn_sched_barrier(0);
-        stage(k0, sKey0, sBs0, sKs0);
+        stage(k0, sKey0, sBs0, sKs0, sBs1, sKs1, n1);
         __builtin_amdgcn_s_waitcnt(vmcnt_only(STAGE_STORES));
         lds_barrier();
         if (k0 + IDX_STAGE >= key_hi)
             break;
-        if (k0 + 2 * IDX_STAGE < key_end)
+        const bool n0 = k0 + 2 * IDX_STAGE < key_end;
+        if (n0)
             issue(k0 + 2 * IDX_STAGE, sKey0, sBs0, sKs0);
         __builtin_amdgcn_sched_barrier(0);
-        stage(k0 + IDX_STAGE, sKey1, sBs1, sKs1);
+        stage(k0 + IDX_STAGE, sKey1, sBs1, sKs1, sBs0, sKs0, n0);
         __builtin_amdgcn_s_waitcnt(vmcnt_only(STAGE_STORES));
         lds_barrier();
     }

@@ -75,14 +75,6 @@ JANUS_DEV uint16_t f32_to_bf16_rne(float f)
     return (uint16_t)(u >> 16);
 }
 
-// (max(x,0), max(y,0)) as a bf16 pair: round to nearest even, then clamp the
-// sign with a packed int16 max (v_cvt_pk_bf16_f32 + v_pk_max_i16).
-JANUS_DEV v2bf relu_bf16x2(float x, float y)
-{
-    v2s p = __builtin_bit_cast(v2s, __builtin_convertvector((v2f){x, y}, v2bf));
-    return __builtin_bit_cast(v2bf, __builtin_elementwise_max(p, (v2s){0, 0}));
-}
-
 // Order-preserving map of an fp32 score to uint32 (larger score -> larger
 // key); -0.0 is folded onto +0.0 so the two compare equal.
 JANUS_DEV uint32_t score_key(float f)

@@ -65,6 +65,29 @@ def test_mxfp4_wide_block_scales_and_key_scale():
     _check_rows(wl, sc.cpu().numpy(), np.arange(wl.total_q, dtype=np.int32), kI, bs)
 
 
+def test_mxfp4_block_scales_differ_within_a_key():
+    """Each 32-element block of a key with its own magnitude (2^-60 .. 2^40,
+    so a key's block scales differ by up to 2^100) and a key scale: the
+    prefill kernel divides each key's block scales by the largest and
+    multiplies it back into the key scale, which must leave every score as
+    the oracle's."""
+    wl = make_workload(hist_len=[2500, 700], new_len=[12, 7], H=64, d=128, idx_dtype="fp8", k=64, seed=78,
+                       w_scale=0.125, key_format="mxfp4")
+    rng = np.random.default_rng(6)
+    kf = rng.standard_normal((wl.total_ctx, 128)).astype(np.float32)
+    kf *= np.repeat(np.exp2(rng.choice([-60.0, -25.0, -5.0, 0.0, 15.0, 40.0], size=(wl.total_ctx, 4))), 32,
+                    axis=1).astype(np.float32)
+    kI, bs = quantize_mxfp4(kf)
+    e = bs.astype(np.int32)
+    assert (e.max(1) - e.min(1)).max() >= 90  # keys with far-apart block scales are present
+    ks = rng.uniform(0.5, 2.0, wl.total_ctx).astype(np.float32)
+    wl.k_scale = ks
+    bt = janus.Batch(wl.hist_len, wl.new_len)
+    sc = janus.index_scores_mxfp4(bt, T(wl.q), T(kI), T(bs), T(wl.w), q_scale=T(wl.q_scale), k_scale=T(ks))
+    torch.cuda.synchronize()
+    _check_rows(wl, sc.cpu().numpy(), np.arange(wl.total_q, dtype=np.int32), kI, bs)
+
+
 def test_mxfp4_decode_batch():
     from workloads import decode_lengths
     M = decode_lengths(12, 4096, 40000, seed=9)
