@@ -268,11 +268,14 @@ int janus_predict_diff(const uint32_t *actual, const uint32_t *predicted,
  *   out     device [total_q, Hq, dv], out_dt JANUS_BF16 or JANUS_F32
  *   lse     device [total_q, Hq] fp32, or NULL
  * A row with no valid id gets out = 0 and lse = -inf.  Softmax and
- * accumulation are fp32; products run on bf16 MFMA for Hq in {16, 32, 64,
- * 128}, dqk = 576, dv = 512, v_pool == k_pool, k <= 4096, a row stride that
- * is a multiple of 8 and at most 2^30, and 16-byte aligned q and pool;
- * otherwise on a plain
- * vector kernel (dqk <= 1024, dv <= 1024), else JANUS_ERR_UNSUPPORTED.
+ * accumulation are fp32; products run on bf16 MFMA for
+ *   - MLA: Hq in {16, 32, 64, 128}, dqk = 576, dv = 512, v_pool == k_pool,
+ *     k <= 4096;
+ *   - MQA: 1 <= Hq <= 16, dqk = dv = 128, k <= 1024 (separate or shared
+ *     pools);
+ * each with row strides that are multiples of 8 and at most 2^30, and
+ * 16-byte aligned q and pools; otherwise on a plain vector kernel
+ * (dqk <= 1024, dv <= 1024), else JANUS_ERR_UNSUPPORTED.
  */
 int janus_sparse_attn(const janus_batch *b,
                       const void *q, int Hq, int dqk, int dv,

@@ -660,6 +660,203 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         }
 }
 
+// MQA kernel for up to 16 query heads with dqk = dv = 128 and separate K and
+// V pools (the attention of the small config: 8 heads sharing one KV head).
+// One wave per query token, four independent waves per block (no block
+// barriers).  A wave holds its token's queries as the B operand of
+// S^T = K Q^T (heads past Hq are zero rows), gathers each 32-key tile's K
+// and V rows straight into its own double-buffered LDS tiles, and needs no
+// P exchange: its S^T lanes hold 8 keys of one head, the A operand of P V.
+// K rows keep 16-byte chunk c at slot c ^ (row & 15), V rows at slot
+// c ^ 2(row & 7), so that the K-operand reads and the transposing V reads
+// touch distinct bank groups; the gather loads each lane's chunk from the
+// pool so that it lands in its swizzled slot.
+constexpr int MQA_D = 128;                     // dqk = dv
+constexpr int MQA_ROWB = MQA_D * 2;            // bytes per K or V row
+constexpr int MQA_TILEB = MLA_KT * MQA_ROWB;   // one 32-row tile (8 KB)
+constexpr int MQA_MAX_K = 1024;                // selected ids per token held in LDS
+constexpr int MQA_WAVES = 4;                   // tokens per block
+
+__global__ __launch_bounds__(64 * MQA_WAVES, 1) void sparse_mqa_mfma(
+    const int32_t *__restrict__ q_start, const int32_t *__restrict__ hist_len, int num_seqs, int es, int total_q,
+    const uint16_t *__restrict__ q, int Hq, const uint8_t *__restrict__ k_pool, const uint8_t *__restrict__ v_pool,
+    int64_t k_row_bytes, int64_t v_row_bytes, const int32_t *__restrict__ page_table, int pt_ld, int page_shift,
+    const int32_t *__restrict__ topk, int k, float scale_log2, void *__restrict__ out, int out_f32,
+    float *__restrict__ lse)
+{
+    // per wave: K and V tiles, two of each (separate arrays, so that the
+    // compiler tells the gathers into one from the reads of the other), and
+    // the token's slots
+    __shared__ __attribute__((aligned(16))) uint8_t sK0[MQA_WAVES][MQA_TILEB];
+    __shared__ __attribute__((aligned(16))) uint8_t sV0[MQA_WAVES][MQA_TILEB];
+    __shared__ __attribute__((aligned(16))) uint8_t sK1[MQA_WAVES][MQA_TILEB];
+    __shared__ __attribute__((aligned(16))) uint8_t sV1[MQA_WAVES][MQA_TILEB];
+    __shared__ int32_t sSlotW[MQA_WAVES][MQA_MAX_K];
+    const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int g = blockIdx.x * MQA_WAVES + wave;
+    if (g >= total_q)
+        return;
+    const int c16 = lane & 15, grp = lane >> 4;
+    const int b = session_of_row(q_start, num_seqs, g);
+    const int lim = last_cand(hist_len[b], g - q_start[b], es);
+    const int32_t *pt = page_table + (int64_t)b * pt_ld;
+    const int32_t *sel = topk + (int64_t)g * k;
+    const int psz_mask = (1 << page_shift) - 1;
+    int32_t *slots = sSlotW[wave];
+    for (int j = lane; j < k; j += 64) {
+        const int s = sel[j];
+        slots[j] = (s >= 0 && s <= lim) ? ((pt[s >> page_shift] << page_shift) + (s & psz_mask)) : -1;
+    }
+    // B operand of S^T = K Q^T: head c16, dims 32*st + 8*grp .. +7
+    v8bf qf[4];
+    {
+        const bool hv = c16 < Hq;
+        const uint16_t *qr = q + ((int64_t)g * Hq + (hv ? c16 : 0)) * MQA_D + 8 * grp;
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+            qf[st] = hv ? as_v8bf(*(const v4i *)(qr + 32 * st)) : as_v8bf(v4i{0, 0, 0, 0});
+    }
+    // O for heads 4*grp + i over dims 16*nb + c16
+    v4f o[8];
+#pragma unroll
+    for (int nb = 0; nb < 8; ++nb)
+        o[nb] = v4f{0.f, 0.f, 0.f, 0.f};
+    float m = -INFINITY, lsum = 0.f;  // head c16
+    __builtin_amdgcn_s_waitcnt(0);     // slots written (this wave reads only its own)
+
+    const int ntiles = (k + MLA_KT - 1) / MLA_KT;
+    // gathers of tile t: instruction i loads rows 4i .. 4i+3 (lane l: row
+    // 4i + l/16, LDS slot l%16, which holds the row's chunk l%16 ^ swizzle)
+    auto issue = [&](int t, uint8_t *__restrict__ kd, uint8_t *__restrict__ vd) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int r = 4 * i + grp;
+            const int j = MLA_KT * t + r;
+            int sl = j < k ? slots[j] : -1;
+            if (sl < 0)
+                sl = 0;  // padding rows read a real row; their logits are masked
+            const int ck = c16 ^ (r & 15), cv = c16 ^ (2 * (r & 7));
+            const uint8_t *ks = k_pool + (uint64_t)(uint32_t)sl * (uint64_t)k_row_bytes + 16 * ck;
+            const uint8_t *vs = v_pool + (uint64_t)(uint32_t)sl * (uint64_t)v_row_bytes + 16 * cv;
+            __builtin_amdgcn_global_load_lds((const void *)ks, (lds_void *)(kd + 1024 * i), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void *)vs, (lds_void *)(vd + 1024 * i), 16, 0, 0);
+        }
+    };
+    if (ntiles > 0)
+        issue(0, sK0[wave], sV0[wave]);
+    // one tile: its K and V tiles (kt, vt) and the buffers (kn, vn) that take
+    // tile t+1's gathers first (they held tile t-1, read in full by now).
+    // All four are restrict-qualified, so that the reads of this tile are not
+    // made to wait for those gathers.
+    auto tile_step = [&](int t, const uint8_t *__restrict__ kt, const uint8_t *__restrict__ vt,
+                         uint8_t *__restrict__ kn, uint8_t *__restrict__ vn) {
+        if (t + 1 < ntiles) {
+            issue(t + 1, kn, vn);
+            __builtin_amdgcn_s_waitcnt(vmcnt_only(16));  // tile t has landed
+        } else {
+            __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+        }
+        // S^T for keys 16*kb + 4*grp + i of head c16
+        v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
+#pragma unroll
+        for (int st = 0; st < 4; ++st) {
+            const int c = 4 * st + grp;
+            const v4i k0 = *(const v4i *)(kt + c16 * MQA_ROWB + 16 * (c ^ c16));
+            const v4i k1 = *(const v4i *)(kt + (16 + c16) * MQA_ROWB + 16 * (c ^ c16));
+            st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(k0), qf[st], st0, 0, 0, 0);
+            st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(k1), qf[st], st1, 0, 0, 0);
+        }
+        const int jr = MLA_KT * t + (lane & 31);
+        const int vslot = jr < k ? slots[jr] : -1;
+        const uint32_t vbits = (uint32_t)__ballot(vslot >= 0);
+        const uint32_t vmask = vbits >> (4 * grp);
+        float x[2][4];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const bool ok = (vmask >> (16 * kb + i)) & 1u;
+                x[kb][i] = ok ? (kb ? st1[i] : st0[i]) * scale_log2 : -INFINITY;
+                mx = fmaxf(mx, x[kb][i]);
+            }
+        const bool over = mx > m + RESCALE_SLACK || (m == -INFINITY && mx > -INFINITY);
+        if (__ballot(over) != 0) {
+            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const bool grow = mx > m + RESCALE_SLACK || (m == -INFINITY && mx > -INFINITY);
+            const float mnew = grow ? mx : m;
+            const float alpha = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mnew);
+            lsum *= alpha;
+            m = mnew;
+            // O rows are heads 4*grp + i: their factors from lanes 4*grp + i
+            float ai[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                ai[i] = __shfl(alpha, 4 * grp + i, 64);
+#pragma unroll
+            for (int nb = 0; nb < 8; ++nb)
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    o[nb][i] *= ai[i];
+        }
+        float pv[2][4];
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                pv[kb][i] = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[kb][i] - m);
+                lsum += pv[kb][i];
+            }
+        const v8bf pa = v8bf{(__bf16)pv[0][0], (__bf16)pv[0][1], (__bf16)pv[0][2], (__bf16)pv[0][3],
+                             (__bf16)pv[1][0], (__bf16)pv[1][1], (__bf16)pv[1][2], (__bf16)pv[1][3]};
+        // V operand: keys 4*grp + j and 16 + 4*grp + j (the P fragment's
+        // order), lane (r' = c16/4, cc = c16%4) addressing dims 16*nb + 4*cc ..
+        const int rr0 = 4 * grp + (c16 >> 2), cc = c16 & 3;
+        const int sw = 2 * (rr0 & 7);  // rr0 + 16 has the same swizzle
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) {
+            const int off = 16 * ((2 * nb + (cc >> 1)) ^ sw) + 8 * (cc & 1);
+            const v4s16 lo = lds_read_tr16(vt, rr0 * MQA_ROWB + off);
+            const v4s16 hi = lds_read_tr16(vt, (rr0 + 16) * MQA_ROWB + off);
+            const v8bf bv = __builtin_bit_cast(v8bf, (v8s16){lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+            o[nb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, bv, o[nb], 0, 0, 0);
+        }
+    };
+    // tile t in buffers t % 2 (the loop unrolled by two)
+    for (int t = 0; t < ntiles; t += 2) {
+        tile_step(t, sK0[wave], sV0[wave], sK1[wave], sV1[wave]);
+        if (t + 1 < ntiles)
+            tile_step(t + 1, sK1[wave], sV1[wave], sK0[wave], sV0[wave]);
+    }
+    float l = lsum;
+    l += __shfl_xor(l, 16, 64);
+    l += __shfl_xor(l, 32, 64);
+    const float inv = l > 0.f ? 1.f / l : 0.f;
+    if (grp == 0 && c16 < Hq && lse)
+        lse[(int64_t)g * Hq + c16] = l > 0.f ? (m + log2f(l)) * LN2 : -INFINITY;
+    float iv[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+        iv[i] = __shfl(inv, 4 * grp + i, 64);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        const int h = 4 * grp + i;
+        if (h >= Hq)
+            continue;
+        const int64_t orow = ((int64_t)g * Hq + h) * MQA_D;
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) {
+            const int d = 16 * nb + c16;
+            const float v = o[nb][i] * iv[i];
+            if (out_f32)
+                ((float *)out)[orow + d] = v;
+            else
+                ((uint16_t *)out)[orow + d] = f32_to_bf16_rne(v);
+        }
+    }
+}
+
 // Merge of a selection split into S slices (flash-decoding): per (token,
 // head), with slice maxima m_s and sums l_s, M = max m_s, w_s = 2^(m_s - M),
 // O = sum_s w_s O_s / sum_s w_s l_s and lse = (M + log2 sum_s w_s l_s) ln 2.
@@ -833,6 +1030,18 @@ static bool mla_shape(const void *q, int Hq, int dqk, int dv, const void *k_pool
            (Hq == 128 || Hq == 64 || Hq == 32 || Hq == 16);
 }
 
+// the MQA shape the MFMA kernel above takes: dqk = dv = 128, at most 16
+// heads, k <= 1024, row strides a multiple of 8 elements, 16-byte aligned q
+// and pools
+static bool mqa_shape(const void *q, int Hq, int dqk, int dv, const void *k_pool, const void *v_pool,
+                      int64_t k_row_stride, int64_t v_row_stride, int k)
+{
+    return dqk == MQA_D && dv == MQA_D && Hq >= 1 && Hq <= 16 && k <= MQA_MAX_K && (k_row_stride % 8) == 0 &&
+           (v_row_stride % 8) == 0 && k_row_stride <= (1 << 30) && v_row_stride <= (1 << 30) &&
+           (reinterpret_cast<uintptr_t>(k_pool) & 15) == 0 && (reinterpret_cast<uintptr_t>(v_pool) & 15) == 0 &&
+           (reinterpret_cast<uintptr_t>(q) & 15) == 0;
+}
+
 // one launch of the MLA kernel: splits blocks per token, each over one slice
 // of the selection (part = NULL: splits = 1, normalised output); pool rows
 // of row_bytes bytes, bf16 or (kv8) fp8 with an inline scale
@@ -968,6 +1177,14 @@ extern "C" int janus_sparse_attn(const janus_batch *bt, const void *q, int Hq, i
     if (mla_shape(q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, k)) {
         launch_mla<false>(bt, q, Hq, k_pool, 2 * k_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32,
                           lse, 1, nullptr, st);
+        return launch_status();
+    }
+    if (mqa_shape(q, Hq, dqk, dv, k_pool, v_pool, k_row_stride, v_row_stride, k)) {
+        hipLaunchKernelGGL(sparse_mqa_mfma, dim3((bt->total_q + MQA_WAVES - 1) / MQA_WAVES), dim3(64 * MQA_WAVES), 0,
+                           st, bt->q_start, bt->hist_len, bt->num_seqs, bt->entry_shift, (int)bt->total_q,
+                           (const uint16_t *)q, Hq, (const uint8_t *)k_pool, (const uint8_t *)v_pool,
+                           2 * k_row_stride, 2 * v_row_stride, page_table, pt_ld, shift, topk_idx, k, sl2, out, of32,
+                           lse);
         return launch_status();
     }
     if (dqk > VEC_MAX_DQK || dv > 4 * VEC_THREADS)

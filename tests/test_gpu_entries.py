@@ -176,11 +176,12 @@ def test_entry_vector_kernels_and_sharded_topk():
     """The generic kernels at entry granularity (E = 8): fp32 indexer scores
     (4 heads x 64), top-k and the sharded top-k on the GPU's own scores (exact
     against the oracle's selection over the same fp32 rows), and MQA attention
-    with separate K and V pools; two sessions, one shorter than an entry."""
+    with separate K and V pools at 24 heads (more than the MQA MFMA kernel
+    takes); two sessions, one shorter than an entry."""
     from workloads.gen import MQA0_ATTN
     E = 8
     wl = make_workload(hist_len=[1500, 5], new_len=[70, 30], H=4, d=64, idx_dtype="f32", k=32, seed=51,
-                       attn=MQA0_ATTN, entry_shift=3, table="permuted", page_size=16)
+                       attn=dict(MQA0_ATTN, Hq=24), entry_shift=3, table="permuted", page_size=16)
     bt = janus.Batch(wl.hist_len, wl.new_len, entry_shift=3)
     sc = janus.index_scores(bt, T(wl.q), T(wl.kI), T(wl.w))
     sel = janus.topk(bt, sc, wl.k)
@@ -221,3 +222,36 @@ def test_entry_vector_kernels_and_sharded_topk():
     assert np.array_equal(np.isneginf(l), np.isneginf(lref))
     assert np.allclose(l[np.isfinite(lref)], lref[np.isfinite(lref)], atol=1e-3)
     assert np.isneginf(lref).any()  # session 2's first tokens have no whole entry
+
+
+def test_entry_mqa_mfma_attention():
+    """The small config's MQA attention (8 heads, dqk = dv = 128, separate K
+    and V pools) on the MFMA kernel at entry granularity (E = 8), with ids
+    of entries not yet whole and a session shorter than one entry."""
+    from workloads.gen import MQA0_ATTN
+    E = 8
+    wl = make_workload(hist_len=[1500, 5], new_len=[70, 30], H=4, d=64, idx_dtype="f32", k=96, seed=52,
+                       attn=MQA0_ATTN, entry_shift=3, table="permuted", page_size=16)
+    bt = janus.Batch(wl.hist_len, wl.new_len, entry_shift=3)
+    ai = attention_inputs(wl)
+    sel = synth_topk(wl, seed=9, hot_frac=0.6, pad_rows=2)
+    rng = np.random.default_rng(2)
+    sel[:, :4] = rng.integers(0, int(wl.ctx_len.max()), size=(wl.total_q, 4))  # some not yet whole
+    out, lse = janus.sparse_attn(bt, T(ai.q), T(ai.k_pool), T(ai.v_pool), T(wl.page_table), wl.page_size, T(sel),
+                                 ai.scale, dv=ai.dv, out_dtype="f32", want_lse=True)
+    torch.cuda.synchronize()
+    rows = np.arange(wl.total_q, dtype=np.int32)
+    ref, lref = oracle.sparse_attn(wl.q_start, wl.hist_len, rows, attention_q_rows(wl, rows), ai.k_pool, ai.v_pool,
+                                   ai.k_row_stride, ai.v_row_stride, wl.page_table, wl.page_size, sel, ai.scale,
+                                   ai.dv, entry=E)
+    got, gl = out.cpu().numpy(), lse.cpu().numpy()
+    assert np.isneginf(lref).any()
+    for j in rows:
+        if np.isneginf(lref[j]).all():  # no whole entry yet
+            assert np.all(got[j] == 0) and np.all(np.isneginf(gl[j])), (j,)
+            continue
+        err = np.abs(got[j] - ref[j]).max()
+        assert err <= 2e-2 and err <= 2e-2 * np.abs(ref[j]).max(), (j, err)
+    fin = np.isfinite(lref)
+    assert np.array_equal(fin, np.isfinite(gl))
+    assert np.allclose(gl[fin], lref[fin], atol=2e-3)

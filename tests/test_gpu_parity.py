@@ -299,9 +299,27 @@ def test_sparse_mla_full_selection_is_dense_and_bf16_out():
     assert np.abs(gb - got).max() <= np.abs(ref).max() * 2 ** -7
 
 
-def test_sparse_attn_vector_mqa():
-    attn = dict(Hq=8, dqk=128, dv=128, mla=False, q_std=1.0, kv_std=1.0, scale=1.0 / math.sqrt(128.0))
-    wl = make_workload(hist_len=[800, 100], new_len=[9, 4], H=2, d=8, idx_dtype="f32", k=300, seed=2, attn=attn)
+@pytest.mark.parametrize("Hq,k", [(8, 300), (1, 64), (16, 1024), (5, 33)])
+def test_sparse_mqa_mfma(Hq, k):
+    """MQA with separate K and V pools at dqk = dv = 128 (the small config's
+    attention: 8 heads sharing one KV head) on the MFMA kernel: one head,
+    16 heads, a ragged tile (k = 33) and the largest k it takes, with padded
+    rows and ids past the causal limit."""
+    attn = dict(Hq=Hq, dqk=128, dv=128, mla=False, q_std=1.0, kv_std=1.0, scale=1.0 / math.sqrt(128.0))
+    wl = make_workload(hist_len=[1800, 100, 0], new_len=[9, 4, 3], H=2, d=8, idx_dtype="f32", k=k, seed=2 + Hq,
+                       table="permuted", attn=attn)
+    sel = synth_topk(wl, seed=5, pad_rows=2)
+    got, ref = _attn_check(wl, attention_inputs(wl), sel)
+    gb, _ = _attn_check(wl, attention_inputs(wl), sel, out_dtype="bf16")
+    assert np.abs(gb - got).max() <= np.abs(ref).max() * 2 ** -7
+
+
+@pytest.mark.parametrize("Hq,dqk,dv,k", [(8, 64, 96, 200), (24, 128, 128, 200), (8, 128, 128, 1100)])
+def test_sparse_attn_vector_kernel(Hq, dqk, dv, k):
+    """Shapes outside the MFMA kernels (other head dims, more than 16 MQA
+    heads, k above 1024 at dqk = 128) run on the plain vector kernel."""
+    attn = dict(Hq=Hq, dqk=dqk, dv=dv, mla=False, q_std=1.0, kv_std=1.0, scale=1.0 / math.sqrt(dqk))
+    wl = make_workload(hist_len=[1500, 100], new_len=[5, 4], H=2, d=8, idx_dtype="f32", k=k, seed=3, attn=attn)
     sel = synth_topk(wl, seed=5, pad_rows=2)
     _attn_check(wl, attention_inputs(wl), sel)
 
