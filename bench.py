@@ -52,6 +52,9 @@ def parse():
                         "(for profiler passes)")
     p.add_argument("--cpu-rows", type=int, default=128, help="query rows in the oracle's multi-threaded sample")
     p.add_argument("--cpu-rows-1t", type=int, default=16, help="query rows in the oracle's single-threaded sample")
+    p.add_argument("--spread-only", action="store_true",
+                   help="time only the attention with selections spread over the whole pool (one JSON field), "
+                        "for the HBM counter passes of that kernel")
     p.add_argument("--c4-layers", type=int, default=8,
                    help="layers of the prediction workload (history 131072 + 4096) in the predicted-path field")
     p.add_argument("--traffic", default=os.path.join(ROOT, "profiles", "index_scores_traffic.json"))
@@ -91,6 +94,10 @@ def main():
     kv = T(ai.k_pool)
     P, ps, k, mr = wl.num_phys_pages, wl.page_size, wl.k, wl.max_run
     N, M = wl.total_q, int(wl.hist_len[0])
+    if args.spread_only:
+        print(json.dumps({"sparse_attn_spread": spread_attention(janus, torch, wl, bt, qa, kv, pt, ai,
+                                                                 max(args.steps, 5))}))
+        return
 
     scores = torch.empty(bt.total_scores, dtype=torch.float32, device=dev)
     sel = torch.empty((N, k), dtype=torch.int32, device=dev)
