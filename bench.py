@@ -43,8 +43,8 @@ PEAK_HBM = 8.0e12      # bytes/s
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=10)
-    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--no-decode", action="store_true", help="skip the decode-phase measurement")
     p.add_argument("--core-only", action="store_true",
@@ -188,6 +188,7 @@ def main():
     share = indexshare_group(janus, torch, step_calls=(bt, q, kI, w, sq, sk, pt, ps, P, mr, k, scores, sel, qa, kv,
                                                        pd_out, diff_out, pred_bm, out, lse, ai),
                              steps=max(args.steps, 3)) if extras else None
+    peaks = measured_peaks(torch) if extras else None
     rec = {
         "metric": "new tokens/s per layer (indexer+top-k+sparse attn) at 128K history; % MFMA/HBM peak",
         "value": N * args.steps / wall,
@@ -226,6 +227,7 @@ def main():
         "decode": decode,
         "indexshare": share,
         "fp8_kv": kv8,
+        "measured_peaks": peaks,
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(wl, ai, args.cpu_rows, args.cpu_rows_1t, sel.cpu().numpy(),
@@ -480,11 +482,86 @@ def predicted_path(janus, torch, layers):
                            "precision": _pct(c[2], c[1]), "miss_pages": c[3], "miss_runs": c[4],
                            "actual_runs": rec["runs"], "kernels_ms": dict(zip(names, map(float, t)))})
     mean = lambda key: float(np.mean([r[key] for r in layers_out]))
+    # the first layer again behind a seeded random page table: the same sets
+    # of pages up to the permutation, but adjacent logical pages are no longer
+    # adjacent physically, so runs shrink to single pages
+    perm = torch.randperm(P, generator=g, device=dev).to(torch.int32).reshape(1, P)
+    x = L[0]
+    janus.index_scores(bt, x["q"], x["kI"], x["w"], q_scale=x["sq"], k_scale=x["sk"], scores=scores)
+    janus.topk(bt, scores, k, out=sel)
+    janus.page_demand(bt, sel, perm, ps, P, mr, out=pd_a)
+    janus.index_scores(bt, x["qp"], x["kI"], x["w"], q_scale=x["sqp"], k_scale=x["sk"], scores=scores)
+    janus.topk(bt, scores, k, out=psel)
+    janus.page_demand(bt, psel, perm, ps, P, mr, out=pd_p)
+    janus.predict_diff(pd_a[0], pd_p[0], P, mr, out=diff)
+    torch.cuda.synchronize()
+    c = diff[2].cpu().tolist()
+    permuted = {"layer": 0, "actual_pages": c[0], "actual_runs": int(pd_a[3][1]), "predicted_pages": c[1],
+                "recall": _pct(c[2], c[0]), "precision": _pct(c[2], c[1]), "miss_pages": c[3], "miss_runs": c[4]}
     return {"workload": f"{layers} layers, history 131072 + 4096 new tokens, k=2048, identity page table, "
                         "q_pred = 0.9 q + sqrt(0.19) N(0,1)",
             "per_layer_actual_ms": mean("actual_path_ms"), "per_layer_predicted_ms": mean("predicted_path_ms"),
             "per_layer_predict_diff_ms": mean("predict_diff_ms"),
-            "prediction_overhead": mean("prediction_overhead"), "layers": layers_out}
+            "prediction_overhead": mean("prediction_overhead"), "layers": layers_out,
+            "permuted_table": permuted}
+
+
+def measured_peaks(torch, reps=5):
+    """What this GPU reaches on plain library work, beside the published
+    peaks the rooflines use: a 2 GiB device copy (HBM read + write) and a sum
+    over the same 2 GiB (read only), and
+    8192^3 GEMMs through hipBLASLt in fp8 e4m3 (torch._scaled_mm, bf16 out)
+    and bf16 (torch.matmul).  Medians of HIP-event timings."""
+    dev = torch.device("cuda:0")
+
+    def timed(f):
+        f()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            f()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return float(np.median(ts)) * 1e-3
+
+    out = {}
+    try:
+        src = torch.empty(1 << 29, dtype=torch.float32, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        t = timed(lambda: dst.copy_(src))
+        out["hbm_copy_TBps"] = 2.0 * src.numel() * 4 / t / 1e12
+        t = timed(lambda: torch.sum(src))
+        out["hbm_read_TBps"] = src.numel() * 4 / t / 1e12
+        del src, dst
+    except RuntimeError as e:
+        out["hbm_copy_TBps"] = None
+        out["hbm_copy_error"] = str(e)[:200]
+    n = 8192
+    try:
+        g = torch.Generator(device=dev)
+        g.manual_seed(0)
+        a = torch.randn((n, n), generator=g, device=dev).to(torch.float8_e4m3fn)
+        b = torch.randn((n, n), generator=g, device=dev).to(torch.float8_e4m3fn).t()
+        one = torch.ones((), device=dev)
+        t = timed(lambda: torch._scaled_mm(a, b, scale_a=one, scale_b=one, out_dtype=torch.bfloat16))
+        out["fp8_gemm_TFLOPs"] = 2.0 * n ** 3 / t / 1e12
+        del a, b
+    except (RuntimeError, AttributeError, TypeError) as e:
+        out["fp8_gemm_TFLOPs"] = None
+        out["fp8_gemm_error"] = str(e)[:200]
+    try:
+        a = torch.randn((n, n), device=dev, dtype=torch.bfloat16)
+        b = torch.randn((n, n), device=dev, dtype=torch.bfloat16)
+        t = timed(lambda: torch.matmul(a, b))
+        out["bf16_gemm_TFLOPs"] = 2.0 * n ** 3 / t / 1e12
+        del a, b
+    except RuntimeError as e:
+        out["bf16_gemm_TFLOPs"] = None
+        out["bf16_gemm_error"] = str(e)[:200]
+    return out
 
 
 def fp8kv_attention(janus, torch, bt, qa, kv, pt, ps, sel, ai, steps, bf16_ms):
