@@ -74,6 +74,22 @@ JANUS_DEV v4s16 lds_read_tr16(const uint8_t *lds_base, int byte_off)
         (lds_v4s16 *)((__attribute__((address_space(3))) uint8_t *)lds_base + byte_off));
 }
 
+// One 16-byte-per-lane gather into LDS (global_load_lds_dwordx4: lane l's
+// 16 bytes from src land at dst + 16 l), written as assembly so that the
+// compiler does not wait for every outstanding LDS read at the next use of
+// any of them, as it does after the builtin.  M0 holds the LDS address (one
+// wait state before the load reads it) and is restored afterwards.
+JANUS_DEV void gather16(const uint8_t *src, uint8_t *dst)
+{
+    const uint32_t m = (uint32_t)(uintptr_t)(lds_void *)dst;
+    int saved;
+    asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, off\n\t"
+                 "s_mov_b32 m0, %0"
+                 : "=&s"(saved)
+                 : "s"(m), "v"(src)
+                 : "memory");
+}
+
 // Every wave issues the same number of gather instructions per tile, so a
 // counted wait is exact; instruction slots past the tile's chunks load a
 // dummy chunk into padding.
@@ -310,7 +326,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         int ln = lane;
         asm volatile("" : "+v"(ln));
         const uint8_t *src = kv + (uint64_t)(uint32_t)sl * (uint32_t)row_bytes + 16 * ln;
-        __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + r * MLA_ROWB), 16, 0, 0);
+        gather16(src, dst + r * MLA_ROWB);
     };
     auto fire_tails = [&](int tt, const int (&ts)[NTAIL], uint8_t *__restrict__ dst) {
         int ln = lane;
@@ -322,8 +338,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             tail_rc(m, ln, r, cc);
             const int sl = (MLA_KT * tt + r < kl && ts[u] >= 0) ? ts[u] : 0;
             const uint8_t *src = kv + (uint64_t)(uint32_t)sl * (uint32_t)row_bytes + 16 * (64 + cc);
-            __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + MLA_TAIL + 1024 * m), 16, 0,
-                                             0);
+            gather16(src, dst + MLA_TAIL + 1024 * m);
         }
     };
     // all of tile tt's gathers at once (the first two tiles)
@@ -395,9 +410,12 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // K operands: 16 bytes (bf16) or 8 bytes (fp8, widened to bf16 in
         // registers) per lane and K-step for keys c16 and c16 + 16.  Q and O
         // fill most of the registers, so the compiler alone keeps too few
-        // operand reads in flight: each step loads the next step's operands
-        // into a two-entry ring, and a scheduling fence per step keeps it
-        // from hoisting more than that
+        // operand reads in flight: each step loads the operands of the step
+        // two ahead (bf16; fp8 rows one ahead) into a ring, and a scheduling
+        // fence per step keeps it from hoisting more than that.  The ring
+        // keeps its reads in flight only because the bf16 gathers are
+        // assembly (gather16): after the builtin the compiler waits for every
+        // outstanding LDS read
         using KRaw = std::conditional_t<KV8, v2i, v4i>;
         constexpr int SB = KV8 ? 32 : 64;  // bytes per K-step
         const uint8_t *row0 = KV8 ? tile + kv8_key_off(c16) + 8 * grp : tile + c16 * MLA_ROWB + 16 * grp;
@@ -424,17 +442,24 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                 return *(const KRaw *)(tile + tail_off((lnk & 15) + 16 * h, 4 * (step - 16) + (lnk >> 4)));
             return *(const KRaw *)((h ? row1 : row0) + SB * step);
         };
-        KRaw ring[2][2];
-        ring[0][0] = kop(0, 0);
-        ring[0][1] = kop(0, 1);
+        // bf16 rows load two steps ahead (a three-entry ring), fp8 rows one
+        constexpr int AHEAD = KV8 ? 1 : 2;
+        KRaw ring[AHEAD + 1][2];
+#pragma unroll
+        for (int a = 0; a < AHEAD; ++a) {
+            ring[a][0] = kop(a, 0);
+            ring[a][1] = kop(a, 1);
+        }
 #pragma unroll
         for (int step = 0; step < MLA_STEPS; ++step) {
-            if (step + 1 < MLA_STEPS) {
-                ring[(step + 1) & 1][0] = kop(step + 1, 0);
-                ring[(step + 1) & 1][1] = kop(step + 1, 1);
+            if (step + AHEAD < MLA_STEPS) {
+                ring[(step + AHEAD) % (AHEAD + 1)][0] = kop(step + AHEAD, 0);
+                ring[(step + AHEAD) % (AHEAD + 1)][1] = kop(step + AHEAD, 1);
             }
-            st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step & 1][0]), qf[step], st0, 0, 0, 0);
-            st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step & 1][1]), qf[step], st1, 0, 0, 0);
+            st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step % (AHEAD + 1)][0]), qf[step], st0, 0, 0,
+                                                          0);
+            st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step % (AHEAD + 1)][1]), qf[step], st1, 0, 0,
+                                                          0);
             // issue points: fp8 at steps 0, 4, .., 16; bf16 at 2, 6, 10, 14
             // and 17, after the slots read at the top of the tile have landed
             if (KV8 ? step % 4 == 0 : (step % 4 == 2 || step == MLA_STEPS - 1))
@@ -592,6 +617,10 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         lds_barrier();
     };
 
+    // the queries have landed before any gather goes out: the compiler does
+    // not count the gathers (assembly), so it must see nothing of its own
+    // outstanding inside the tile loop
+    __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
     if (ntiles > 0)
         issue_all(0, sKV0);
     if (ntiles > 1)
