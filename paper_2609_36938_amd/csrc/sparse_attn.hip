@@ -256,7 +256,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             if (slot < 0)
                 slot = 0;  // padding rows read a real row; their logits are masked
             const uint8_t *src = kv + (uint64_t)(uint32_t)slot * (uint32_t)row_bytes + 16 * c;
-            __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
+            gather16(src, dst + (64 * j) * 16);
         }
     };
 
@@ -281,7 +281,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             const int j = wave + NW * (I0 + u);
             const int sl = slot[u] < 0 ? 0 : slot[u];  // padding rows read a real row; their logits are masked
             const uint8_t *src = kv + (uint64_t)(uint32_t)sl * (uint32_t)row_bytes + 16 * cc[u];
-            __builtin_amdgcn_global_load_lds((const void *)src, (lds_void *)(dst + (64 * j) * 16), 16, 0, 0);
+            gather16(src, dst + (64 * j) * 16);
         }
     };
     constexpr bool SPREAD8 = KV8 && IPW >= 2;
@@ -411,11 +411,10 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // registers) per lane and K-step for keys c16 and c16 + 16.  Q and O
         // fill most of the registers, so the compiler alone keeps too few
         // operand reads in flight: each step loads the operands of the step
-        // two ahead (bf16; fp8 rows one ahead) into a ring, and a scheduling
-        // fence per step keeps it from hoisting more than that.  The ring
-        // keeps its reads in flight only because the bf16 gathers are
-        // assembly (gather16): after the builtin the compiler waits for every
-        // outstanding LDS read
+        // two ahead into a ring, and a scheduling fence per step keeps it from
+        // hoisting more than that.  The ring keeps its reads in flight only
+        // because the gathers are assembly (gather16): after the builtin the
+        // compiler waits for every outstanding LDS read
         using KRaw = std::conditional_t<KV8, v2i, v4i>;
         constexpr int SB = KV8 ? 32 : 64;  // bytes per K-step
         const uint8_t *row0 = KV8 ? tile + kv8_key_off(c16) + 8 * grp : tile + c16 * MLA_ROWB + 16 * grp;
@@ -442,8 +441,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                 return *(const KRaw *)(tile + tail_off((lnk & 15) + 16 * h, 4 * (step - 16) + (lnk >> 4)));
             return *(const KRaw *)((h ? row1 : row0) + SB * step);
         };
-        // bf16 rows load two steps ahead (a three-entry ring), fp8 rows one
-        constexpr int AHEAD = KV8 ? 1 : 2;
+        // two steps ahead: a three-entry ring
+        constexpr int AHEAD = 2;
         KRaw ring[AHEAD + 1][2];
 #pragma unroll
         for (int a = 0; a < AHEAD; ++a) {
@@ -767,8 +766,8 @@ __global__ __launch_bounds__(64 * MQA_WAVES, 1) void sparse_mqa_mfma(
             const int ck = c16 ^ (r & 15), cv = c16 ^ (2 * (r & 7));
             const uint8_t *ks = k_pool + (uint64_t)(uint32_t)sl * (uint64_t)k_row_bytes + 16 * ck;
             const uint8_t *vs = v_pool + (uint64_t)(uint32_t)sl * (uint64_t)v_row_bytes + 16 * cv;
-            __builtin_amdgcn_global_load_lds((const void *)ks, (lds_void *)(kd + 1024 * i), 16, 0, 0);
-            __builtin_amdgcn_global_load_lds((const void *)vs, (lds_void *)(vd + 1024 * i), 16, 0, 0);
+            gather16(ks, kd + 1024 * i);
+            gather16(vs, vd + 1024 * i);
         }
     };
     if (ntiles > 0)
