@@ -47,6 +47,10 @@ constexpr int MLA_TILE_CH = MLA_KT * MLA_PCH;   // chunks per tile (2368)
 constexpr int MLA_TILE_INS = (MLA_TILE_CH + 63) / 64;  // wave-instructions per tile (37)
 constexpr int MLA_MAX_K = 4096;                 // selected ids per token held in LDS
 constexpr float RESCALE_SLACK = 8.0f;           // log2 headroom before O is rescaled
+// Running max before any valid logit: finite and below every logit, so that
+// the rescale test needs no special case and exp2(x - m) of a padding key
+// (x = -inf) is 0.
+constexpr float M_INIT = -3.0e38f;
 
 typedef short v4s16 __attribute__((ext_vector_type(4)));
 
@@ -65,6 +69,26 @@ JANUS_DEV void lds_barrier()
 }
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4s16 lds_v4s16;
+
+// Largest of the 8 MFMA results in a (with b): v_max3 on the raw results.
+// The compiler puts a canonicalizing max in front of each MFMA result it
+// passes to fmaxf; written as assembly the reduction is four instructions,
+// after the wait states a VALU read of an MFMA result needs (the compiler
+// inserts none ahead of inline assembly).
+JANUS_DEV float max8(const v4f &a, const v4f &b)
+{
+    float x, y;
+    asm("s_nop 7\n\ts_nop 7\n\t"
+        "v_max3_f32 %0, %2, %3, %4\n\t"
+        "v_max3_f32 %1, %5, %6, %7"
+        : "=&v"(x), "=&v"(y)
+        : "v"(a[0]), "v"(a[1]), "v"(a[2]), "v"(a[3]), "v"(b[0]), "v"(b[1]));
+    float z;
+    asm("v_max3_f32 %0, %1, %2, %3\n\tv_max3_f32 %0, %0, %4, %5"
+        : "=&v"(z)
+        : "v"(x), "v"(y), "v"(a[3]), "v"(b[2]), "v"(b[3]));
+    return z;
+}
 
 // Transposing LDS read (ds_read_b64_tr_b16): within each 16-lane group,
 // lane i's element j is element i%4 of the 8 bytes addressed by lane 4j+i/4.
@@ -104,6 +128,9 @@ constexpr int KV8_GAP = 8;                               // chunks between keys 
 constexpr int KV8_TILE_CH = MLA_KT * KV8_CPR + KV8_GAP;  // 1192
 constexpr int KV8_SCALE = MLA_DQK;                       // byte of the scale in a row
 JANUS_DEV int kv8_key_off(int r) { return r * KV8_ROWB + (r >= 16 ? KV8_GAP * 16 : 0); }
+// K-step at which a tile's key scales are read (their LDS latency passes
+// under the remaining steps; at the last step it showed in the softmax)
+constexpr int KS_STEP = 10;
 
 // bf16 rows in a tile buffer: dims 0..511 of key row r ("main", 1 KB) at
 // r * MLA_ROWB, so that one gather instruction loads one row and its source
@@ -237,7 +264,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
 #pragma unroll
         for (int nl = 0; nl < NBW; ++nl)
             o[hb][nl] = v4f{0.f, 0.f, 0.f, 0.f};
-    float m = -INFINITY, lsum = 0.f;  // head head0 + c16
+    float m = M_INIT, lsum = 0.f;  // head head0 + c16
     __syncthreads();
 
     const int ntiles = (kl + MLA_KT - 1) / MLA_KT;
@@ -405,6 +432,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         if constexpr (!KV8)
             read_slots(t + 2, vs, ts);
         int vslot;
+        float ks[2][4];  // fp8 rows: scales of keys 16*kb + 4*grp + i
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
         v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
         // K operands: 16 bytes (bf16) or 8 bytes (fp8, widened to bf16 in
@@ -466,6 +494,15 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             // this tile's slots (for its valid keys), read under the last MFMAs
             if (step == MLA_STEPS - 1)
                 vslot = sSlot[min(MLA_KT * t + (lane & 31), kl - 1)];
+            if constexpr (KV8) {
+                if (step == KS_STEP) {
+#pragma unroll
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            ks[kb][i] = *(const float *)(tile + kv8_key_off(16 * kb + 4 * grp + i) + KV8_SCALE);
+                }
+            }
             __builtin_amdgcn_sched_barrier(0);
         }
         if constexpr (KV8)
@@ -479,20 +516,12 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // positive scale - takes the max over the raw products and one fma
         // per probability, with no masks
         const bool fast = !KV8 && vbits == 0xFFFFFFFFu && scale_log2 > 0.f;
-        // fp8 rows: each key's scale multiplies its logit and its probability
-        float ks[2][4];
-        if constexpr (KV8) {
-#pragma unroll
-            for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    ks[kb][i] = *(const float *)(tile + kv8_key_off(16 * kb + 4 * grp + i) + KV8_SCALE);
-        }
+        // fp8 rows: each key's scale (ks, read from step KS_STEP on)
+        // multiplies its logit and its probability
         float x[2][4];
         float mx = -INFINITY;
         if (fast) {
-            mx = scale_log2 * fmaxf(fmaxf(fmaxf(st0[0], st0[1]), fmaxf(st0[2], st0[3])),
-                                    fmaxf(fmaxf(st1[0], st1[1]), fmaxf(st1[2], st1[3])));
+            mx = scale_log2 * max8(st0, st1);
         } else {
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -507,14 +536,14 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // the running max m is common to a head's four lane groups; it only
         // moves when some key exceeds it by the slack, which is rare after
         // the first tiles, so the cross-lane reduction runs only then
-        const bool over = mx > m + RESCALE_SLACK || (m == -INFINITY && mx > -INFINITY);
+        const bool over = mx > m + RESCALE_SLACK;
         const bool resc = __ballot(over) != 0;
         if (resc) {
             mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
             mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-            const bool grow = mx > m + RESCALE_SLACK || (m == -INFINITY && mx > -INFINITY);
+            const bool grow = mx > m + RESCALE_SLACK;
             const float mnew = grow ? mx : m;
-            const float alpha = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m - mnew);
+            const float alpha = __builtin_amdgcn_exp2f(m - mnew);
             lsum *= alpha;
             m = mnew;
             if (grp == 0)
@@ -537,7 +566,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    pv[kb][i] = (m == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(x[kb][i] - m);
+                    pv[kb][i] = __builtin_amdgcn_exp2f(x[kb][i] - m);
                     lsum += pv[kb][i];
                     if constexpr (KV8)  // V_s = scale_s * (stored row); padding keys stay 0
                         pv[kb][i] = ((vmask >> (16 * kb + i)) & 1u) ? pv[kb][i] * ks[kb][i] : 0.f;
@@ -641,7 +670,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         l += __shfl_xor(l, 32, 64);
         if (grp == 0) {
             float *ml = part + (int64_t)gridDim.x * HQ * MLA_DV + ((int64_t)blockIdx.x * HQ + head0 + c16) * 2;
-            ml[0] = m;
+            ml[0] = l > 0.f ? m : -INFINITY;  // an empty slice: -inf, as the merge expects
             ml[1] = l;
         }
 #pragma unroll
