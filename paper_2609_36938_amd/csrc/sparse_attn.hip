@@ -70,6 +70,17 @@ JANUS_DEV void lds_barrier()
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4s16 lds_v4s16;
 
+// The lane id made inside the code that uses it: the compiler can neither
+// hoist it out of a rarely taken branch nor keep it live (and spill it)
+// across the tile loop.
+JANUS_DEV int lane_here()
+{
+    int ln;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(ln));
+    return ln;
+}
+
+
 // Largest of the 8 MFMA results in a (with b): v_max3 on the raw results.
 // The compiler puts a canonicalizing max in front of each MFMA result it
 // passes to fmaxf; written as assembly the reduction is four instructions,
@@ -511,7 +522,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // of the tile come as a 32-bit mask (lanes 32-63 repeat 0-31); this
         // lane's keys are 16*kb + 4*grp + i
         const uint32_t vbits = (uint32_t)__ballot(MLA_KT * t + (lane & 31) < kl && vslot >= 0);
-        const uint32_t vmask = vbits >> (4 * grp);
+        const uint32_t vmask = vbits >> (4 * (KV8 ? grp : lane_here() >> 4));
         // the common case - every key of the tile valid, bf16 rows and a
         // positive scale - takes the max over the raw products and one fma
         // per probability, with no masks
@@ -539,15 +550,18 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         const bool over = mx > m + RESCALE_SLACK;
         const bool resc = __ballot(over) != 0;
         if (resc) {
-            mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-            mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+            const int ln = lane_here();
+            mx = fmaxf(mx, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((ln ^ 16) << 2,
+                                                                                  __builtin_bit_cast(int, mx))));
+            mx = fmaxf(mx, __builtin_bit_cast(float, __builtin_amdgcn_ds_bpermute((ln ^ 32) << 2,
+                                                                                  __builtin_bit_cast(int, mx))));
             const bool grow = mx > m + RESCALE_SLACK;
             const float mnew = grow ? mx : m;
             const float alpha = __builtin_amdgcn_exp2f(m - mnew);
             lsum *= alpha;
             m = mnew;
-            if (grp == 0)
-                sAlpha[head0 + c16] = alpha;
+            if (ln < 16)
+                sAlpha[head0 + ln] = alpha;
         }
         if (lane == 0)
             sResc[wave] = resc;
