@@ -1077,7 +1077,9 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
                        : 1.0f;
     };
     auto compute = [&](int g, const Group &G) {
-        float res[NQ][4];
+        // one vector per token, so that picking this lane's key below is a
+        // register select (an array of floats picked by kg goes to scratch)
+        v4f res[NQ];
         // (fp8 serves decode only: a group past every limit is rare there)
         const bool masked = FP4 && c0 + 64 * g > last_lim;  // block-uniform
 #pragma unroll
@@ -1107,7 +1109,7 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
         for (int t = 0; t < NQ; ++t) {
             if (t >= nv)
                 continue;
-            float v = kg == 0 ? res[t][0] : kg == 1 ? res[t][1] : kg == 2 ? res[t][2] : res[t][3];
+            float v = res[t][kg];
             v = s > lim[t] ? -INFINITY : v * G.ks;
             const uint32_t off = s < ctx ? (uint32_t)(t * ctx + s) * 4u : 0x80000000u;
             __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), srs, off, 0, 0);
