@@ -18,6 +18,10 @@ FLAGS = [
     "-I" + os.path.join(ROOT, "include"), "-I" + CSRC,
     # packed fp32 VALU ops are kept out of every kernel
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # loops marked for full unrolling are unrolled whatever their size: past
+    # the default limit the one-wave fp8-row attention kernels kept their
+    # K-step loop rolled and indexed their queries in scratch memory
+    "-mllvm", "-pragma-unroll-threshold=200000",
     "-Wall", "-Wno-unused-function",
 ]
 

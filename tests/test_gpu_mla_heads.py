@@ -1,0 +1,80 @@
+"""MLA attention (Sec. 2.2: one latent KV row of 576 dims shared by all
+heads, the values its first 512) at the head counts that one tensor-parallel
+shard of the 128-head layer holds: 16, 32 and 64 heads, which run one, two
+and four waves per block.  bf16 and fp8 rows (Sec. 5.1), whole and split over
+slices, against the oracle on every row.  Tolerances as for 128 heads: max
+abs err <= 2e-2 and <= 2e-2 of the row's largest output, lse to 2e-3; rows
+with no valid id give zeros and -inf.  The large-logit case (scale 8) moves
+the running max in later tiles, so the lazy rescale runs."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from workloads import attention_inputs, attention_kv_fp8, attention_q_rows, make_workload, synth_topk
+from workloads.gen import MLA_ATTN
+
+pytestmark = pytest.mark.gpu
+janus = pytest.importorskip("paper_2609_36938_amd")
+
+
+def T(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+CASES = [(16, 1.0 / 24.0, 1.0 / 24.0), (32, 1.0 / 24.0, 1.0 / 24.0), (64, 1.0 / 24.0, 1.0 / 24.0),
+         (16, 1.0 / 24.0, 8.0), (64, 1.0 / 24.0, 8.0)]
+
+
+@pytest.fixture(scope="module", params=CASES, ids=lambda c: f"H{c[0]}-scale{c[2]:g}")
+def case(request):
+    Hq, kv_std, scale = request.param
+    attn = dict(MLA_ATTN, Hq=Hq, kv_std=kv_std, scale=scale)
+    wl = make_workload(hist_len=[1500, 300], new_len=[6, 5], H=2, d=8, idx_dtype="f32", k=200, seed=50 + Hq,
+                       table="permuted", attn=attn)
+    sel = synth_topk(wl, seed=7, pad_rows=2)
+    sel[wl.q_start[1], :] = -1  # a row with no valid id
+    return wl, attention_inputs(wl), sel
+
+
+def _compare(got, gl, ref, lref):
+    for r in range(ref.shape[0]):
+        if np.isneginf(lref[r]).all():
+            assert np.all(got[r] == 0) and np.all(np.isneginf(gl[r])), (r,)
+            continue
+        err = np.abs(got[r] - ref[r]).max()
+        assert err <= 2e-2 and err <= 2e-2 * np.abs(ref[r]).max(), (r, err)
+    fin = np.isfinite(lref)
+    assert np.array_equal(fin, np.isfinite(gl))
+    assert np.allclose(gl[fin], lref[fin], atol=2e-3)
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+def test_mla_bf16_heads(case, splits):
+    wl, ai, sel = case
+    bt = janus.Batch(wl.hist_len, wl.new_len)
+    kv = T(ai.k_pool)
+    args = (bt, T(ai.q), kv, kv, T(wl.page_table), wl.page_size, T(sel), ai.scale)
+    if splits == 1:
+        out, lse = janus.sparse_attn(*args, dv=ai.dv, out_dtype="f32", want_lse=True)
+    else:
+        out, lse = janus.sparse_attn_split(*args, num_splits=splits, dv=ai.dv, out_dtype="f32", want_lse=True)
+    torch.cuda.synchronize()
+    rows = np.arange(wl.total_q)
+    ref, lref = oracle.sparse_attn(wl.q_start, wl.hist_len, rows, ai.q, ai.k_pool, None, ai.k_row_stride,
+                                   ai.k_row_stride, wl.page_table, wl.page_size, sel, ai.scale, ai.dv)
+    _compare(out.cpu().numpy(), lse.cpu().numpy(), ref, lref)
+
+
+@pytest.mark.parametrize("splits", [1, 3])
+def test_mla_fp8_heads(case, splits):
+    wl, ai, sel = case
+    pool8 = attention_kv_fp8(wl)
+    bt = janus.Batch(wl.hist_len, wl.new_len)
+    out, lse = janus.sparse_attn_fp8kv(bt, T(ai.q), T(pool8), T(wl.page_table), wl.page_size, T(sel), ai.scale,
+                                       num_splits=splits, out_dtype="f32", want_lse=True)
+    torch.cuda.synchronize()
+    rows = np.arange(wl.total_q, dtype=np.int32)
+    ref, lref = oracle.sparse_attn_fp8kv(wl.q_start, wl.hist_len, rows, attention_q_rows(wl, rows), pool8,
+                                         wl.page_table, wl.page_size, sel[rows], ai.scale, entry=1)
+    _compare(out.cpu().numpy(), lse.cpu().numpy(), ref, lref)
