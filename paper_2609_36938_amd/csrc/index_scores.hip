@@ -2,33 +2,32 @@
 //   S[i,s] = sq[i] * sk[s] * sum_h w[i,h] * max(0, q[i,h,:] . kI[s,:]),  s <= M+i
 //
 // fp8 path (d = 128): one v_mfma_f32_16x16x128_f8f6f4 covers a whole 128-dim
-// dot product, so each MFMA is a 16 (token,head) x 16 key tile and the only
+// dot product, so each MFMA is a 16 (token, head) x 16 key tile and the only
 // reduction left is the ReLU-weighted sum over heads, done in the epilogue.
-// The 16 MFMA rows are 4 tokens x 4 heads, ordered so that output rows
-// 4g..4g+3 of every tile belong to token g: each lane then owns one
-// (token, key) score and sums all H heads in registers, with no cross-lane
-// reduction.  A wave keeps its 4 tokens' queries (4 x H x 128 fp8) resident
-// in VGPRs and streams 16-key operand blocks straight from L2; the column
-// of block j is key s0 + 4c + j, so after 4 blocks a lane holds 4 adjacent
-// keys and stores them as one 16-byte write (256 contiguous bytes per token).
-// Key blocks wholly past every token's causal limit skip the MFMAs.
+// The prefill kernel keeps each wave's two tokens' queries (2 x H x 128 fp8)
+// in VGPRs and streams the keys through LDS; the row-tile kernel (decode
+// shapes, MXFP4 keys) reads its keys straight from global memory.
 //
 // Epilogue: the MFMA applies an E8M0 scale of 2^-25 to the query operand, so
 // every product lands in (-1, 1): |q.k| <= 128 * 448 * 448 < 2^25 for any
 // e4m3 inputs.  On that range the clamping form of v_cvt_pk_bf16_f32 (which
 // clamps to [0, 1] after rounding to nearest even) is exactly ReLU followed
-// by the bf16 rounding, so each pair of outputs costs one convert and one
-// v_dot2_f32_bf16 against head weights pre-multiplied by 2^25: 4 VALU ops
-// per 16x16x128 MFMA.  The fp8 MFMA and the VALU do not overlap on this
-// chip, so VALU ops per MFMA bound the kernel.  Every term is non-negative,
-// so the two bf16 roundings bound the relative error of a score by 2^-8.
+// by the bf16 rounding, with head weights pre-multiplied by 2^25.  The fp8
+// MFMA and the VALU do not overlap on this chip, so VALU work per MFMA bounds
+// the kernels.  The row-tile kernel dots each converted pair with its weights
+// (v_dot2c_f32_bf16): 4 VALU ops per MFMA.  The prefill kernel feeds the
+// converted pairs to a bf16 MFMA whose A operand holds the weights, which
+// sums the heads of a token across lanes as well: 2 VALU ops per fp8 MFMA
+// and one bf16 MFMA per two, which other waves' VALU work overlaps.  Every
+// term is non-negative, so the two bf16 roundings bound the relative error
+// of a score by 2^-8.
 //
 // The clamp modifier cannot be requested from the compiler, so the convert
 // is inline assembly; the compiler does not insert the wait states a VALU
-// read of an MFMA result needs ahead of inline assembly, so the four MFMAs
-// of a group are issued from one assembly block that ends with the wait
-// states (12 for an 8-pass fp8 MFMA, what the compiler itself emits) and
-// starts with the one a VALU write of an MFMA source needs.
+// read of an MFMA result needs ahead of inline assembly, so the MFMAs of a
+// group are issued from one assembly block that carries its own wait states
+// (12 for an 8-pass fp8 MFMA, what the compiler itself emits) and starts
+// with the one a VALU write of an MFMA source needs.
 #include "janus_device.hpp"
 #include "janus_host.hpp"
 
@@ -125,6 +124,53 @@ JANUS_DEV void head_group(float &acc, const v8i &a0, const v8i &a1, const v8i &a
             : [acc] "+v"(acc)
             : IDX_HEAD_GROUP_INPUTS
             : IDX_HEAD_GROUP_CLOBBERS);
+}
+
+// The group of four head tiles with the weighted head sum on a bf16 MFMA
+// (the prefill kernel's form).  After the four fp8 MFMAs each pair of
+// outputs is clamped to [0, 1] and rounded to bf16 - ReLU, as above - and
+// packed so that v[112:115] holds tiles 0 and 1 and v[116:119] tiles 2 and
+// 3: lane group g's eight bf16 are rows 4g..4g+3 of the first tile, then of
+// the second, at the lane's key.  That is the B operand (32 slots x 16 keys)
+// of v_mfma_f32_16x16x32_bf16, whose A operand (wp0, wp1) holds the head
+// weights of each slot in the row of the slot's token and zeros elsewhere,
+// so the MFMA adds up a token's weighted heads across the lane groups.  The
+// converts cost one VALU instruction per two outputs, and a bf16 MFMA,
+// unlike an fp8 one, leaves most of its cycles to the VALU work of the other
+// waves.  Wait states: the converts read MFMA k's result 16, 14, 12 and 12
+// wait states after it (each later 8-pass MFMA counted as four); the
+// head-sum MFMAs read the packed operands two or more after their last write
+// and accumulate back to back; eight pad the end, before anything reads hc.
+// FIRST starts the sum at zero.
+#define IDX_HEAD_SUM(C0)                                                                              \
+    "s_nop 1\n\t" IDX_MFMA("v[112:115]", "a0") IDX_MFMA("v[116:119]", "a1") IDX_MFMA("v[120:123]", "a2")  \
+        IDX_MFMA("v[124:127]", "a3")                                                                  \
+    "s_nop 3\n\t"                                                                                     \
+    "v_cvt_pk_bf16_f32 v112, v112, v113 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v113, v114, v115 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v114, v116, v117 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v115, v118, v119 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v116, v120, v121 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v117, v122, v123 clamp\n\t"                                                    \
+    "s_nop 1\n\t"                                                                                     \
+    "v_cvt_pk_bf16_f32 v118, v124, v125 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v119, v126, v127 clamp\n\t"                                                    \
+    "s_nop 1\n\t"                                                                                     \
+    "v_mfma_f32_16x16x32_bf16 %[hc], %[wp0], v[112:115], " C0 "\n\t"                                 \
+    "v_mfma_f32_16x16x32_bf16 %[hc], %[wp1], v[116:119], %[hc]\n\t"                                  \
+    "s_nop 7"
+#define IDX_HEAD_SUM_INPUTS                                                                            \
+    [a0] "v"(a0), [a1] "v"(a1), [a2] "v"(a2), [a3] "v"(a3), [bk] "v"(bk), [sc] "v"(scales), [wp0] "v"(wp0), \
+        [wp1] "v"(wp1)
+
+template <bool FIRST>
+JANUS_DEV void head_sum_group(v4f &hc, const v8i &a0, const v8i &a1, const v8i &a2, const v8i &a3, const v8i &bk,
+                              int scales, const v8bf &wp0, const v8bf &wp1)
+{
+    if (FIRST)
+        asm(IDX_HEAD_SUM("0") : [hc] "=&v"(hc) : IDX_HEAD_SUM_INPUTS : IDX_HEAD_GROUP_CLOBBERS);
+    else
+        asm(IDX_HEAD_SUM("%[hc]") : [hc] "+v"(hc) : IDX_HEAD_SUM_INPUTS : IDX_HEAD_GROUP_CLOBBERS);
 }
 
 // The same group with MXFP4 keys, after expand_e2m1 has widened them to fp8
@@ -309,12 +355,12 @@ JANUS_DEV bool xcd_tile_chunk(int L, int nchunks, int ntiles, int &tile, int &ch
 // c ^ ((r >> 1) & 7), so the 16 rows read by one 16-lane group land in 16
 // different bank groups.
 //
-// TPW tokens per wave: an MFMA tile's 16 rows are TPW tokens x RPT = 16/TPW
-// heads, ordered so that output rows 4g..4g+3 (lane group g) hold one token
-// (g*TPW/4) and 4 consecutive heads.  A lane sums its heads in registers; the
-// 4/TPW lane groups that share a token are then added across lanes.  Fewer
-// tokens per wave means fewer registers and more waves per SIMD, whose VALU
-// epilogues then run under the other waves' MFMAs.
+// Two tokens per wave: an MFMA tile's 16 rows are 2 tokens x 8 heads,
+// ordered so that output rows 4g..4g+3 (lane group g) hold token g/2 and 4
+// consecutive heads.  The head-sum MFMA adds a token's heads over its two
+// lane groups and over each pair of tiles, and returns token t's sums of the
+// 16 keys in lane group t.  Two tokens per wave keep the registers at 128,
+// for four waves per SIMD.
 template <int H, int TPW>
 __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma(
     const int32_t *__restrict__ q_start, const int32_t *__restrict__ ctx_start,
@@ -323,6 +369,8 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     const uint8_t *__restrict__ kI, const float *__restrict__ k_scale, const float *__restrict__ w,
     float *__restrict__ scores)
 {
+    // the head sums come out in rows 0 and 4 of the head-sum MFMA: two tokens of 8 heads per tile
+    static_assert(TPW == 2 && H % 16 == 0, "two tokens per wave");
     constexpr int RPT = 16 / TPW;   // heads of one token per MFMA tile
     constexpr int HB = H / RPT;     // MFMA tiles per 16-key block
     constexpr int TOK_TILE = 4 * TPW;
@@ -400,35 +448,45 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
     const int64_t e_row = (int64_t)qrow0 + (e_ok ? e_tok : 0);
     const int hsub = (4 * kg) % RPT;
     // head weights times the token's query scale (a positive factor of every
-    // term) and 2^25 (undoing the MFMA's query scale), rounded once to bf16 pairs
+    // term) and 2^25 (undoing the MFMA's query scale), rounded once to bf16.
+    // The head-sum MFMA's A operand of tile pair p (tiles 2p, 2p+1): row
+    // 4*(kg/2) is token kg/2's, and lane (kg, r16 = 4*(kg/2)) holds the
+    // weights of the heads in its slots (those of rows 4kg..4kg+3 of each
+    // tile); every other lane holds zeros.
     const float sq = (q_scale ? q_scale[e_row] : 1.0f) * 0x1p25f;
-    v2bf wv[HB][2];
+    const bool hs_lane = r16 == 4 * (kg >> 1);
+    v8bf wA[HB / 2];
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        v4f t = *(const v4f *)(w + e_row * H + RPT * hb + hsub);
-        wv[hb][0] = __builtin_convertvector((v2f){t[0] * sq, t[1] * sq}, v2bf);
-        wv[hb][1] = __builtin_convertvector((v2f){t[2] * sq, t[3] * sq}, v2bf);
+    for (int p = 0; p < HB / 2; ++p) {
+        const v4f t0 = *(const v4f *)(w + e_row * H + RPT * (2 * p) + hsub);
+        const v4f t1 = *(const v4f *)(w + e_row * H + RPT * (2 * p + 1) + hsub);
+        const float f = hs_lane ? sq : 0.0f;
+        wA[p] = __builtin_convertvector((v8f){t0[0] * f, t0[1] * f, t0[2] * f, t0[3] * f, t1[0] * f, t1[1] * f,
+                                              t1[2] * f, t1[3] * f},
+                                        v8bf);
     }
-    const int lim = last_cand(M, e_tok, es);  // last causal candidate of this lane's token
     const int wave_lim = last_cand(M, min(tw0 + TPW - 1, N - 1), es);
     int scales = IDX_MFMA_SCALES;
     // this lane's two 16-byte columns (2*kg, 2*kg+1) of LDS row 16*j + r16
     const int g8 = (r16 >> 1) & 7;
     const int off0 = r16 * 128 + 16 * ((2 * kg) ^ g8), off1 = r16 * 128 + 16 * ((2 * kg + 1) ^ g8);
-    // lanes sharing a token split the stores: group-in-token index
-    constexpr int GPT = 4 / TPW;            // lane groups per token
-    const int gin = kg % GPT;
-    // Scores leave through buffer stores over this block's rows: a lane with
-    // nothing to write uses an offset past the range and the hardware drops
-    // it, so every wave issues the same number of stores per full stage and
-    // the stage can wait for its key prefetch with vmcnt(STAGE_STORES)
+    // The head sums land in row 4t of the head-sum MFMA's output for token
+    // tw0 + t: lane group t (lanes 16t .. 16t+15) holds token t's sums of the
+    // block's 16 keys in element 0, and one store per 16-key block writes
+    // them for both tokens.  Scores leave through buffer stores over this
+    // block's rows: a lane with nothing to write (lane groups 2 and 3, or a
+    // token past the tile) uses an offset past the range and the hardware
+    // drops it, so every wave issues the same number of stores per full stage
+    // and the stage can wait for its key prefetch with vmcnt(STAGE_STORES)
     // instead of draining the stores.
+    const int s_tok = tw0 + kg;
     const int nrows_blk = max(0, min(TOK_TILE, N - tile0));
     const int64_t blk_off = score_start[b] + (int64_t)tile0 * ctx;
     const __amdgpu_buffer_rsrc_t rsrc = make_buffer_rsrc(scores + blk_off, (uint32_t)((int64_t)nrows_blk * ctx * 4));
-    const bool row_ok = e_ok && wave_on;
-    const uint32_t lane_row_off = (uint32_t)((int64_t)(e_tok - tile0) * ctx * 4);
-    constexpr int STORES_PER_GROUP = 4 / GPT;
+    const bool row_ok = kg < TPW && s_tok < N && wave_on;
+    const uint32_t lane_row_off = (uint32_t)((int64_t)(s_tok - tile0) * ctx * 4);
+    const int lim = last_cand(M, s_tok, es);  // last causal candidate of this lane's token
+    constexpr int STORES_PER_GROUP = 4;
     constexpr int STAGE_STORES = (IDX_STAGE / 64) * STORES_PER_GROUP;
     // every token of the block sees all keys below this bound
     const int interior_end = min(ctx, last_cand(M, tile0, es) + 1);
@@ -440,40 +498,25 @@ __global__ __launch_bounds__(256, (TPW == 4 ? 2 : 4)) void index_scores_fp8_mfma
             const int s0 = k0 + 64 * gsub;
             if (s0 >= key_hi)
                 break;
-            float res[4];
             const bool skip = !wave_on || s0 > wave_lim;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (skip) {
-                    res[j] = -INFINITY;
-                    continue;
+            for (int j = 0; j < STORES_PER_GROUP; ++j) {
+                // token tw0 + kg at key s0 + 16*j + r16 (kg < 2), before the key scale
+                float v = -INFINITY;
+                if (!skip) {
+                    const uint8_t *rowb = stg + (64 * gsub + 16 * j) * 128;
+                    v4i lo = *(const v4i *)(rowb + off0), hi = *(const v4i *)(rowb + off1);
+                    const v8i bk = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+                    v4f hc;
+                    head_sum_group<true>(hc, a[0], a[1], a[2], a[3], bk, scales, wA[0], wA[1]);
+#pragma unroll
+                    for (int h4 = 4; h4 < HB; h4 += 4)
+                        head_sum_group<false>(hc, a[h4], a[h4 + 1], a[h4 + 2], a[h4 + 3], bk, scales, wA[h4 / 2],
+                                              wA[h4 / 2 + 1]);
+                    v = hc[0];
                 }
-                const uint8_t *rowb = stg + (64 * gsub + 16 * j) * 128;
-                v4i lo = *(const v4i *)(rowb + off0), hi = *(const v4i *)(rowb + off1);
-                const v8i bk = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-                float r;
-                head_group<true>(r, a[0], a[1], a[2], a[3], bk, scales, &wv[0]);
-#pragma unroll
-                for (int h4 = 4; h4 < HB; h4 += 4)
-                    head_group<false>(r, a[h4], a[h4 + 1], a[h4 + 2], a[h4 + 3], bk, scales, &wv[h4]);
-                if (GPT >= 2)
-                    r += xor_lanes16(r);
-                if (GPT >= 4)
-                    r += __shfl_xor(r, 32, 64);
-                res[j] = r;
-            }
-            // res[j] is token e_tok at key s0 + 16*j + r16 (before the key
-            // scale); the GPT lane groups of a token hold the same values and
-            // take turns, so each store instruction writes with every lane
-#pragma unroll
-            for (int js = 0; js < STORES_PER_GROUP; ++js) {
-                float v = res[js * GPT];
-#pragma unroll
-                for (int u = 1; u < GPT; ++u)
-                    v = gin == u ? res[js * GPT + u] : v;
-                const int jj = js * GPT + gin;
-                const int s = s0 + 16 * jj + r16;
-                const float kscale = k_scale ? ks[64 * gsub + 16 * jj + r16] : 1.0f;
+                const int s = s0 + 16 * j + r16;
+                const float kscale = k_scale ? ks[64 * gsub + 16 * j + r16] : 1.0f;
                 uint32_t off;
                 if (s0 + 64 <= interior_end) {  // block-uniform: no causal or range checks
                     v *= kscale;

@@ -43,8 +43,45 @@ v_dot2c_f32_bf16 v93, v126, v73
 s_nop 2""".splitlines()
 
 
+# the prefill kernel's group with the head sum on a bf16 MFMA (accumulating form)
+GOOD_HS = """s_nop 1
+v_mfma_scale_f32_16x16x128_f8f6f4 v[112:115], v[42:49], v[98:105], 0, v96, v96 op_sel:[0,1,0] op_sel_hi:[0,0,0]
+v_mfma_scale_f32_16x16x128_f8f6f4 v[116:119], v[34:41], v[98:105], 0, v96, v96 op_sel:[0,1,0] op_sel_hi:[0,0,0]
+v_mfma_scale_f32_16x16x128_f8f6f4 v[120:123], v[58:65], v[98:105], 0, v96, v96 op_sel:[0,1,0] op_sel_hi:[0,0,0]
+v_mfma_scale_f32_16x16x128_f8f6f4 v[124:127], v[50:57], v[98:105], 0, v96, v96 op_sel:[0,1,0] op_sel_hi:[0,0,0]
+s_nop 3
+v_cvt_pk_bf16_f32 v112, v112, v113 clamp
+v_cvt_pk_bf16_f32 v113, v114, v115 clamp
+v_cvt_pk_bf16_f32 v114, v116, v117 clamp
+v_cvt_pk_bf16_f32 v115, v118, v119 clamp
+v_cvt_pk_bf16_f32 v116, v120, v121 clamp
+v_cvt_pk_bf16_f32 v117, v122, v123 clamp
+s_nop 1
+v_cvt_pk_bf16_f32 v118, v124, v125 clamp
+v_cvt_pk_bf16_f32 v119, v126, v127 clamp
+s_nop 1
+v_mfma_f32_16x16x32_bf16 v[82:85], v[74:77], v[112:115], v[82:85]
+v_mfma_f32_16x16x32_bf16 v[82:85], v[78:81], v[116:119], v[82:85]
+s_nop 7""".splitlines()
+
+
 def test_rules_accept_the_documented_group():
     assert check_block(GOOD) == []
+    assert check_block(GOOD_HS) == []
+
+
+@pytest.mark.parametrize("old,new,expect", [
+    ("s_nop 3", "s_nop 2", "12"),                                        # converts read the last MFMAs early
+    ("v_cvt_pk_bf16_f32 v119, v126, v127 clamp\ns_nop 1", "v_cvt_pk_bf16_f32 v119, v126, v127 clamp",
+     "(< 2)"),                                                           # MFMA reads a fresh convert
+    ("\ns_nop 7", "", "4-pass MFMA"),                                    # head sum read right after the block
+    ("v[116:119], v[82:85]", "v[116:119], v[83:86]", "(< 8)"),           # not an exact accumulation
+])
+def test_rules_flag_the_head_sum_group(old, new, expect):
+    text = "\n".join(GOOD_HS)
+    assert old in text
+    bad = check_block(text.replace(old, new, 1).splitlines())
+    assert any(expect in v for v in bad), bad
 
 
 @pytest.mark.parametrize("drop,expect", [
@@ -77,9 +114,10 @@ def test_compiled_indexer_blocks(tmp_path):
     r = subprocess.run(cmd, capture_output=True, text=True)
     assert r.returncode == 0, r.stderr[-2000:]
     bl = [b for b in blocks(out.read_text()) if any(l.startswith("v_mfma") for l in b)]
-    # fp8 groups (prefill and row kernels), the widened MXFP4 group, and the
-    # MXFP4 prefill group with fp4 B operands
+    # fp8 groups (prefill with bf16 head sums, and row kernels), the widened
+    # MXFP4 group, and the MXFP4 prefill group with fp4 B operands
     assert len(bl) >= 4
     assert any("blgp:4" in l for b in bl for l in b)
+    assert any("v_mfma_f32_16x16x32_bf16" in l for b in bl for l in b)
     bad = [v for b in bl for v in check_block(b)]
     assert not bad, "\n".join(bad[:20])
