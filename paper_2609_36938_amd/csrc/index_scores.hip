@@ -203,56 +203,45 @@ JANUS_DEV void head_sum_group(v4f &hc, const v8i &a0, const v8i &a1, const v8i &
         [w00] "v"(w[0][0]), [w01] "v"(w[0][1]), [w10] "v"(w[1][0]), [w11] "v"(w[1][1]), [w20] "v"(w[2][0]), \
         [w21] "v"(w[2][1]), [w30] "v"(w[3][0]), [w31] "v"(w[3][1])
 
-// The fp8 group above with e2m1 keys as the B operand (blgp 4: 16 bytes per
-// lane, lane group g holding the key's elements 32g .. 32g+31, MX block g)
-// and separate scales: sa = 2^-25 for the queries, sb = the lane's block
-// scale divided by the largest of its key's four (so at most 1).  Every
-// product then stays below 128 * 448 * 6 * 2^-25 < 1 in magnitude and the
-// clamping convert is ReLU, as in the fp8 group; the wait states are the fp8
-// group's (the same 8-pass MFMA), with one more after the fourth MFMA.
+// The MXFP4 prefill group: the fp8 prefill group (head sums on a bf16 MFMA)
+// with e2m1 keys as the B operand (blgp 4: 16 bytes per lane, lane group g
+// holding the key's elements 32g .. 32g+31, MX block g) and separate scales:
+// sa = 2^-25 for the queries, sb = the lane's block scale divided by the
+// largest of its key's four (so at most 1).  Every product then stays below
+// 128 * 448 * 6 * 2^-25 < 1 in magnitude and the clamping convert is ReLU,
+// as in the fp8 group; the wait states are the fp8 group's (the same 8-pass
+// MFMA), with one more after the fourth MFMA.
 #define IDX_MFMA_F4C(dst, a) \
     "v_mfma_scale_f32_16x16x128_f8f6f4 " dst ", %[" a "], %[bk], 0, %[sa], %[sb] op_sel_hi:[0,0,0] blgp:4\n\t"
-#define IDX_HEAD_GROUP_F4C(INIT)                                                                     \
-    INIT "s_nop 1\n\t" IDX_MFMA_F4C("v[112:115]", "a0") IDX_MFMA_F4C("v[116:119]", "a1")            \
-        IDX_MFMA_F4C("v[120:123]", "a2") IDX_MFMA_F4C("v[124:127]", "a3")                          \
-    "s_nop 1\n\t"                                                                                     \
+#define IDX_HEAD_SUM_F4C(C0)                                                                          \
+    "s_nop 1\n\t" IDX_MFMA_F4C("v[112:115]", "a0") IDX_MFMA_F4C("v[116:119]", "a1")                  \
+        IDX_MFMA_F4C("v[120:123]", "a2") IDX_MFMA_F4C("v[124:127]", "a3")                            \
+    "s_nop 4\n\t"                                                                                     \
     "v_cvt_pk_bf16_f32 v112, v112, v113 clamp\n\t"                                                    \
-    "v_cvt_pk_bf16_f32 v114, v114, v115 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v112, %[w00]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v116, v116, v117 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v114, %[w01]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v118, v118, v119 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v116, %[w10]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v120, v120, v121 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v118, %[w11]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v122, v122, v123 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v120, %[w20]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v124, v124, v125 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v122, %[w21]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v126, v126, v127 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v124, %[w30]\n\t"                                                       \
-    "s_nop 0\n\t"                                                                                     \
-    "v_dot2c_f32_bf16 %[acc], v126, %[w31]\n\t"                                                       \
-    "s_nop 2"
-#define IDX_HEAD_GROUP_F4C_INPUTS                                                                      \
+    "v_cvt_pk_bf16_f32 v113, v114, v115 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v114, v116, v117 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v115, v118, v119 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v116, v120, v121 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v117, v122, v123 clamp\n\t"                                                    \
+    "s_nop 1\n\t"                                                                                     \
+    "v_cvt_pk_bf16_f32 v118, v124, v125 clamp\n\t"                                                    \
+    "v_cvt_pk_bf16_f32 v119, v126, v127 clamp\n\t"                                                    \
+    "s_nop 1\n\t"                                                                                     \
+    "v_mfma_f32_16x16x32_bf16 %[hc], %[wp0], v[112:115], " C0 "\n\t"                                 \
+    "v_mfma_f32_16x16x32_bf16 %[hc], %[wp1], v[116:119], %[hc]\n\t"                                  \
+    "s_nop 7"
+#define IDX_HEAD_SUM_F4C_INPUTS                                                                        \
     [a0] "v"(a0), [a1] "v"(a1), [a2] "v"(a2), [a3] "v"(a3), [bk] "v"(bk), [sa] "v"(sa), [sb] "v"(sb),   \
-        [w00] "v"(w[0][0]), [w01] "v"(w[0][1]), [w10] "v"(w[1][0]), [w11] "v"(w[1][1]), [w20] "v"(w[2][0]), \
-        [w21] "v"(w[2][1]), [w30] "v"(w[3][0]), [w31] "v"(w[3][1])
+        [wp0] "v"(wp0), [wp1] "v"(wp1)
 
 template <bool FIRST>
-JANUS_DEV void head_group_f4c(float &acc, const v8i &a0, const v8i &a1, const v8i &a2, const v8i &a3, const v4i &bk,
-                              int sa, int sb, const v2bf (*w)[2])
+JANUS_DEV void head_sum_group_f4c(v4f &hc, const v8i &a0, const v8i &a1, const v8i &a2, const v8i &a3,
+                                  const v4i &bk, int sa, int sb, const v8bf &wp0, const v8bf &wp1)
 {
     if (FIRST)
-        asm(IDX_HEAD_GROUP_F4C("v_mov_b32 %[acc], 0\n\t")
-            : [acc] "=&v"(acc)
-            : IDX_HEAD_GROUP_F4C_INPUTS
-            : IDX_HEAD_GROUP_CLOBBERS);
+        asm(IDX_HEAD_SUM_F4C("0") : [hc] "=&v"(hc) : IDX_HEAD_SUM_F4C_INPUTS : IDX_HEAD_GROUP_CLOBBERS);
     else
-        asm(IDX_HEAD_GROUP_F4C("")
-            : [acc] "+v"(acc)
-            : IDX_HEAD_GROUP_F4C_INPUTS
-            : IDX_HEAD_GROUP_CLOBBERS);
+        asm(IDX_HEAD_SUM_F4C("%[hc]") : [hc] "+v"(hc) : IDX_HEAD_SUM_F4C_INPUTS : IDX_HEAD_GROUP_CLOBBERS);
 }
 constexpr int IDX_SCALE_2M25 = 127 - 25;  // E8M0 2^-25
 
@@ -854,32 +843,36 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
         a[hb] = v8i{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
     }
     // output rows 4kg..4kg+3 of every tile: token tw0 + 4kg/RPT, heads
-    // RPT*hb + (4kg)%RPT + i; bf16 weights times the token's query scale
+    // RPT*hb + (4kg)%RPT + i.  Head weights times the token's query scale and
+    // 2^25 (undoing the MFMA's query scale), rounded once to bf16, as the
+    // head-sum MFMA's A operands (as in the fp8 prefill kernel)
     const int e_tok = tw0 + (4 * kg) / RPT;
     const bool e_ok = e_tok < N;
     const int64_t e_row = (int64_t)qrow0 + (e_ok ? e_tok : 0);
     const int hsub = (4 * kg) % RPT;
-    // head weights times the token's query scale and 2^25 (undoing the
-    // MFMA's query scale), rounded once to bf16 pairs
     const float sq = (q_scale ? q_scale[e_row] : 1.0f) * 0x1p25f;
-    v2bf wv[HB][2];
+    const bool hs_lane = r16 == 4 * (kg >> 1);
+    v8bf wA[HB / 2];
 #pragma unroll
-    for (int hb = 0; hb < HB; ++hb) {
-        const v4f t = *(const v4f *)(w + e_row * H + RPT * hb + hsub);
-        wv[hb][0] = __builtin_convertvector((v2f){t[0] * sq, t[1] * sq}, v2bf);
-        wv[hb][1] = __builtin_convertvector((v2f){t[2] * sq, t[3] * sq}, v2bf);
+    for (int p = 0; p < HB / 2; ++p) {
+        const v4f t0 = *(const v4f *)(w + e_row * H + RPT * (2 * p) + hsub);
+        const v4f t1 = *(const v4f *)(w + e_row * H + RPT * (2 * p + 1) + hsub);
+        const float f = hs_lane ? sq : 0.0f;
+        wA[p] = __builtin_convertvector((v8f){t0[0] * f, t0[1] * f, t0[2] * f, t0[3] * f, t1[0] * f, t1[1] * f,
+                                              t1[2] * f, t1[3] * f},
+                                        v8bf);
     }
     const int sa = IDX_SCALE_2M25;
-    const int lim = last_cand(M, e_tok, es);
     const int wave_lim = last_cand(M, min(tw0 + TPW - 1, N - 1), es);
-    constexpr int GPT = 4 / TPW;
-    const int gin = kg % GPT;
+    // token tw0 + t's sums come out in lane group t (t < 2): one store per 16-key block
+    const int s_tok = tw0 + kg;
+    const int lim = last_cand(M, s_tok, es);
     const int nrows_blk = max(0, min(TOK_TILE, N - tile0));
     const int64_t blk_off = score_start[b] + (int64_t)tile0 * ctx;
     const __amdgpu_buffer_rsrc_t rsrc = make_buffer_rsrc(scores + blk_off, (uint32_t)((int64_t)nrows_blk * ctx * 4));
-    const bool row_ok = e_ok && wave_on;
-    const uint32_t lane_row_off = (uint32_t)((int64_t)(e_tok - tile0) * ctx * 4);
-    constexpr int STORES_PER_GROUP = 4 / GPT;
+    const bool row_ok = kg < TPW && s_tok < N && wave_on;
+    const uint32_t lane_row_off = (uint32_t)((int64_t)(s_tok - tile0) * ctx * 4);
+    constexpr int STORES_PER_GROUP = 4;
     constexpr int STAGE_STORES = (IDX_STAGE / 64) * STORES_PER_GROUP;
     const int interior_end = min(ctx, last_cand(M, tile0, es) + 1);
     // this lane's B chunk (key row r16 of a 16-key block, bytes 16kg ..)
@@ -895,32 +888,22 @@ __global__ __launch_bounds__(256, 4) void index_scores_mxfp4_mfma(
             const int s0 = k0 + 64 * gsub;
             if (s0 >= key_hi)
                 break;
-            float res[4];
             const bool skip = !wave_on || s0 > wave_lim;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (skip) {
-                    res[j] = -INFINITY;
-                    continue;
+            for (int j = 0; j < STORES_PER_GROUP; ++j) {
+                // token tw0 + kg at key s0 + 16*j + r16 (kg < 2), before the key scale
+                float v = -INFINITY;
+                if (!skip) {
+                    const int row = 64 * gsub + 16 * j;  // first key of the 16-key block
+                    const v4i bk = *(const v4i *)(stg + row * F4_ROW + boff);
+                    const int sb = (int)((bs[row + r16] >> (8 * kg)) & 0xFFu);  // normalised E8M0 of block kg
+                    v4f hc;
+                    head_sum_group_f4c<true>(hc, a[0], a[1], a[2], a[3], bk, sa, sb, wA[0], wA[1]);
+                    head_sum_group_f4c<false>(hc, a[4], a[5], a[6], a[7], bk, sa, sb, wA[2], wA[3]);
+                    v = hc[0];
                 }
-                const int row = 64 * gsub + 16 * j;  // first key of the 16-key block
-                const v4i bk = *(const v4i *)(stg + row * F4_ROW + boff);
-                const int sb = (int)((bs[row + r16] >> (8 * kg)) & 0xFFu);  // normalised E8M0 of block kg
-                float r;
-                head_group_f4c<true>(r, a[0], a[1], a[2], a[3], bk, sa, sb, &wv[0]);
-                head_group_f4c<false>(r, a[4], a[5], a[6], a[7], bk, sa, sb, &wv[4]);
-                r += xor_lanes16(r);
-                res[j] = r;
-            }
-#pragma unroll
-            for (int js = 0; js < STORES_PER_GROUP; ++js) {
-                float v = res[js * GPT];
-#pragma unroll
-                for (int u = 1; u < GPT; ++u)
-                    v = gin == u ? res[js * GPT + u] : v;
-                const int jj = js * GPT + gin;
-                const int s = s0 + 16 * jj + r16;
-                const float kscale = ks[64 * gsub + 16 * jj + r16];
+                const int s = s0 + 16 * j + r16;
+                const float kscale = ks[64 * gsub + 16 * j + r16];
                 uint32_t off;
                 if (s0 + 64 <= interior_end) {
                     v *= kscale;
