@@ -65,83 +65,30 @@ constexpr int IDX_MFMA_SCALES = 0x7f66;
 // One group of four head tiles against one 16-key block: four 16x16x128
 // fp8 MFMAs sharing the key operand (query scale 2^-25, so every product is
 // below 1 in magnitude), then each pair of outputs clamped to [0, 1] and
-// rounded to bf16 in place - ReLU - and dotted with its bf16 head-weight
-// pair into acc.  The MFMA results live in v[112:127], declared clobbered, so
-// the group is one block whose wait states are written out (the counts the
-// compiler itself emits for these pairs of instructions): two ahead of the
-// MFMAs (a VALU write of one of their sources); twelve between an 8-pass MFMA
-// and the VALU that reads its result, where each later 8-pass MFMA counts as
-// four (so one wait state after the fourth MFMA covers every read below: the
-// second MFMA's first convert comes three instructions later, the fourth's
-// eleven); at least one between a convert and the dot
-// product that reads its pair (each dot reads a pair converted two
-// instructions earlier; consecutive dots accumulating into one register need
-// none), and three at the end, before any other instruction reads the dot
-// product's result.  FIRST starts the accumulator at zero.
+// rounded to bf16 - ReLU - and the weighted head sum on a bf16 MFMA.  The
+// converts pack the outputs so that v[112:115] holds tiles 0 and 1 and
+// v[116:119] tiles 2 and 3: lane group g's eight bf16 are rows 4g..4g+3 of
+// the first tile, then of the second, at the lane's key.  That is the B
+// operand (32 slots x 16 keys) of v_mfma_f32_16x16x32_bf16, whose A operand
+// (wp0, wp1) holds the head weights of each slot in the row of the slot's
+// token and zeros elsewhere, so the MFMA adds up a token's weighted heads
+// across the lane groups.  The converts cost one VALU instruction per two
+// outputs, and a bf16 MFMA, unlike an fp8 one, leaves most of its cycles to
+// the VALU work of the other waves.  The MFMA results live in v[112:127],
+// declared clobbered, so the group is one block whose wait states are
+// written out (the counts the compiler itself emits for these pairs of
+// instructions): two ahead of the MFMAs (a VALU write of one of their
+// sources); twelve between an 8-pass MFMA and a VALU read of its result,
+// where each later 8-pass MFMA counts as four, so the converts read MFMA k's
+// result 16, 14, 12 and 12 wait states after it; two or more between a
+// convert and the head-sum MFMA that reads it; none between two dependent
+// head-sum MFMAs; eight at the end, before anything reads hc.  FIRST starts
+// the sum at zero.
 #define IDX_MFMA(dst, a) \
     "v_mfma_scale_f32_16x16x128_f8f6f4 " dst ", %[" a "], %[bk], 0, %[sc], %[sc] op_sel:[0,1,0] op_sel_hi:[0,0,0]\n\t"
-#define IDX_HEAD_GROUP(INIT)                                                                         \
-    INIT "s_nop 1\n\t" IDX_MFMA("v[112:115]", "a0") IDX_MFMA("v[116:119]", "a1") IDX_MFMA("v[120:123]", "a2") \
-        IDX_MFMA("v[124:127]", "a3")                                                                  \
-    "s_nop 0\n\t"                                                                                     \
-    "v_cvt_pk_bf16_f32 v112, v112, v113 clamp\n\t"                                                    \
-    "v_cvt_pk_bf16_f32 v114, v114, v115 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v112, %[w00]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v116, v116, v117 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v114, %[w01]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v118, v118, v119 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v116, %[w10]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v120, v120, v121 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v118, %[w11]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v122, v122, v123 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v120, %[w20]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v124, v124, v125 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v122, %[w21]\n\t"                                                       \
-    "v_cvt_pk_bf16_f32 v126, v126, v127 clamp\n\t"                                                    \
-    "v_dot2c_f32_bf16 %[acc], v124, %[w30]\n\t"                                                       \
-    "s_nop 0\n\t"                                                                                     \
-    "v_dot2c_f32_bf16 %[acc], v126, %[w31]\n\t"                                                       \
-    "s_nop 2"
-#define IDX_HEAD_GROUP_INPUTS                                                                          \
-    [a0] "v"(a0), [a1] "v"(a1), [a2] "v"(a2), [a3] "v"(a3), [bk] "v"(bk), [sc] "v"(scales),            \
-        [w00] "v"(w[0][0]), [w01] "v"(w[0][1]), [w10] "v"(w[1][0]), [w11] "v"(w[1][1]), [w20] "v"(w[2][0]), \
-        [w21] "v"(w[2][1]), [w30] "v"(w[3][0]), [w31] "v"(w[3][1])
 #define IDX_HEAD_GROUP_CLOBBERS                                                                       \
     "v112", "v113", "v114", "v115", "v116", "v117", "v118", "v119", "v120", "v121", "v122", "v123", "v124", \
         "v125", "v126", "v127"
-
-template <bool FIRST>
-JANUS_DEV void head_group(float &acc, const v8i &a0, const v8i &a1, const v8i &a2, const v8i &a3, const v8i &bk,
-                          int scales, const v2bf (*w)[2])
-{
-    if (FIRST)
-        asm(IDX_HEAD_GROUP("v_mov_b32 %[acc], 0\n\t")
-            : [acc] "=&v"(acc)
-            : IDX_HEAD_GROUP_INPUTS
-            : IDX_HEAD_GROUP_CLOBBERS);
-    else
-        asm(IDX_HEAD_GROUP("")
-            : [acc] "+v"(acc)
-            : IDX_HEAD_GROUP_INPUTS
-            : IDX_HEAD_GROUP_CLOBBERS);
-}
-
-// The group of four head tiles with the weighted head sum on a bf16 MFMA
-// (the prefill kernel's form).  After the four fp8 MFMAs each pair of
-// outputs is clamped to [0, 1] and rounded to bf16 - ReLU, as above - and
-// packed so that v[112:115] holds tiles 0 and 1 and v[116:119] tiles 2 and
-// 3: lane group g's eight bf16 are rows 4g..4g+3 of the first tile, then of
-// the second, at the lane's key.  That is the B operand (32 slots x 16 keys)
-// of v_mfma_f32_16x16x32_bf16, whose A operand (wp0, wp1) holds the head
-// weights of each slot in the row of the slot's token and zeros elsewhere,
-// so the MFMA adds up a token's weighted heads across the lane groups.  The
-// converts cost one VALU instruction per two outputs, and a bf16 MFMA,
-// unlike an fp8 one, leaves most of its cycles to the VALU work of the other
-// waves.  Wait states: the converts read MFMA k's result 16, 14, 12 and 12
-// wait states after it (each later 8-pass MFMA counted as four); the
-// head-sum MFMAs read the packed operands two or more after their last write
-// and accumulate back to back; eight pad the end, before anything reads hc.
-// FIRST starts the sum at zero.
 #define IDX_HEAD_SUM(C0)                                                                              \
     "s_nop 1\n\t" IDX_MFMA("v[112:115]", "a0") IDX_MFMA("v[116:119]", "a1") IDX_MFMA("v[120:123]", "a2")  \
         IDX_MFMA("v[124:127]", "a3")                                                                  \
@@ -173,12 +120,12 @@ JANUS_DEV void head_sum_group(v4f &hc, const v8i &a0, const v8i &a1, const v8i &
         asm(IDX_HEAD_SUM("%[hc]") : [hc] "+v"(hc) : IDX_HEAD_SUM_INPUTS : IDX_HEAD_GROUP_CLOBBERS);
 }
 
-// The same group with MXFP4 keys, after expand_e2m1 has widened them to fp8
-// (sa = 2^6 undoes its 2^-6, sb is the lane's E8M0 block scale).  Block
-// scales can make a product of any size, so ReLU is not folded into the
-// convert here: each pair is rounded to bf16, its sign clamped with a packed
-// int16 max (a negative bf16 is a negative int16), and dotted with the
-// weights.  Convert, max and dot of a pair are at least two instructions apart
+// The row-tile kernel's group with MXFP4 keys, after expand_e2m1 has widened
+// them to fp8 (sa = 2^6 undoes its 2^-6, sb is the lane's E8M0 block scale).
+// Block scales can make a product of any size, so ReLU is not folded into
+// the convert here: each pair is rounded to bf16, its sign clamped with a
+// packed int16 max (a negative bf16 is a negative int16), and dotted with
+// its weights into acc (v_dot2c); the lane groups' sums are added afterwards.  Convert, max and dot of a pair are at least two instructions apart
 // (one wait state after a VALU write read by a packed op).
 #define IDX_MFMA_F4(dst, a) \
     "v_mfma_scale_f32_16x16x128_f8f6f4 " dst ", %[" a "], %[bk], 0, %[sa], %[sb] op_sel_hi:[0,0,0]\n\t"
@@ -987,17 +934,20 @@ __global__ __launch_bounds__(256) void index_scores_vector(
 namespace janus {
 
 // Row-tile kernel: a block takes up to NQ tokens of one session and one
-// chunk of 1024, 2048 or 4096 keys (chosen per launch).  It serves decode-shaped batches (every session appends at
-// most NQ tokens, as in the decode phase: the scores are a GEMV over each
-// session's keys, bound by reading the keys once) and MXFP4 keys at any size.
-// The four waves take the chunk's 64-key groups in turn; a wave reads a
-// group's keys (and their scales) straight from global memory one group ahead
-// - each key is used by this block alone, so nothing is staged in LDS - and
-// for every token runs one head group per 16-key block: four 16x16x128 MFMAs
-// (16 heads x 16 keys each) and the epilogue.  Lane group g then stores
-// 16-key block g of the group: one 256-byte store per token and group.
-// Groups wholly past every token's causal limit skip the MFMAs (their stores
-// write -inf).
+// chunk of 1024, 2048 or 4096 keys (chosen per launch).  It serves
+// decode-shaped batches (every session appends at most NQ tokens, as in the
+// decode phase: the scores are a GEMV over each session's keys, bound by
+// reading the keys once), with fp8 or MXFP4 keys.  The four waves take the
+// chunk's 64-key groups in turn; a wave reads a group's keys (and their
+// scales) straight from global memory one group ahead - each key is used by
+// this block alone, so nothing is staged in LDS - and for every token runs
+// one head group per 16-key block: four 16x16x128 MFMAs (16 heads x 16 keys
+// each) and the epilogue.  fp8 keys: the tokens' head sums accumulate into
+// one head-sum MFMA result whose lane group t holds token t's scores, and
+// one store per 16-key block writes them.  MXFP4 keys: each token's head sum
+// is completed across lanes, and lane group g stores 16-key block g of the
+// group: one 256-byte store per token and group; groups wholly past every
+// token's causal limit skip the MFMAs (their stores write -inf).
 constexpr int ROWS_NQ = 4;
 constexpr int ROWS_CHUNK_MAX = 4096;   // keys per block: 4096, 2048 or 1024
 constexpr int ROWS_CHUNK_MIN = 1024;
@@ -1030,7 +980,11 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
     // 16hb + 4kg + i, whose weights (times the query scale, and for fp8 keys
     // times 2^25) it holds
     v8i a[NQ][4];
-    v2bf wv[NQ][4][2];
+    v2bf wv[NQ][4][2];  // MXFP4 keys: the dot products' weight pairs
+    // fp8 keys: the head-sum MFMA's A operands, tile pairs (0, 1) and (2, 3)
+    // of token t in row 4t (lanes with r16 = 4t; zeros elsewhere), so that
+    // lane group t receives token t's sums (as in the prefill kernel)
+    v8bf wA[NQ][2];
     // MXFP4: the scaled MFMA takes K 16kg .. 16kg+15 from this lane's low 16
     // bytes, K 64+16kg .. from its high 16, and the E8M0 scale of K block b
     // (32 elements) from lane group b.  Lane group kg therefore holds half kg%2
@@ -1052,9 +1006,22 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
             } else {
                 a[t][hb] = ok ? *(const v8i *)(qr + 32 * kg) : v8i{0, 0, 0, 0, 0, 0, 0, 0};
             }
-            const v4f tw = *(const v4f *)(w + row * 64 + 16 * hb + 4 * kg);
-            wv[t][hb][0] = __builtin_convertvector((v2f){tw[0] * sq, tw[1] * sq}, v2bf);
-            wv[t][hb][1] = __builtin_convertvector((v2f){tw[2] * sq, tw[3] * sq}, v2bf);
+            if constexpr (FP4) {
+                const v4f tw = *(const v4f *)(w + row * 64 + 16 * hb + 4 * kg);
+                wv[t][hb][0] = __builtin_convertvector((v2f){tw[0] * sq, tw[1] * sq}, v2bf);
+                wv[t][hb][1] = __builtin_convertvector((v2f){tw[2] * sq, tw[3] * sq}, v2bf);
+            }
+        }
+        if constexpr (!FP4) {
+            const float f = r16 == 4 * t ? sq : 0.0f;
+#pragma unroll
+            for (int p = 0; p < 2; ++p) {
+                const v4f t0w = *(const v4f *)(w + row * 64 + 16 * (2 * p) + 4 * kg);
+                const v4f t1w = *(const v4f *)(w + row * 64 + 16 * (2 * p + 1) + 4 * kg);
+                wA[t][p] = __builtin_convertvector((v8f){t0w[0] * f, t0w[1] * f, t0w[2] * f, t0w[3] * f, t1w[0] * f,
+                                                         t1w[1] * f, t1w[2] * f, t1w[3] * f},
+                                                   v8bf);
+            }
         }
     }
     constexpr int KB = FP4 ? 64 : 128;  // key bytes
@@ -1075,11 +1042,12 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
     for (int t = 0; t < NQ; ++t)
         lim[t] = __builtin_amdgcn_readfirstlane(last_cand(M, t0 + t, es));
     const int last_lim = last_cand(M, t0 + nv - 1, es);  // largest causal limit in the tile
+    const int lane_lim = last_cand(M, t0 + kg, es);       // fp8 keys: the causal limit of the token this lane stores
 
     struct Group {
         v4i k[8];   // 16-key block j: key row 16j + r16; fp8: bytes 32kg.. in k[2j], k[2j+1]; fp4: both halves in k[j]
         int bs[4];  // fp4: the E8M0 scales of key row 16j + r16, block kg in the low byte
-        float ks;   // scale of key 16kg + r16 (the one this lane stores)
+        float ks[4];  // fp4: [0] = scale of key 16kg + r16 (the one this lane stores); fp8: key 16j + r16
     };
     auto load = [&](int g, Group &G) {
         const uint32_t row0 = (uint32_t)(64 * g + r16);
@@ -1098,47 +1066,73 @@ __global__ __launch_bounds__(256, 2) void index_scores_rows(
                 G.k[2 * j + 1] = __builtin_bit_cast(v4i, __builtin_amdgcn_raw_buffer_load_b128(krs, off + 16u, 0, 0));
             }
         }
-        G.ks = k_scale ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
-                                                       ksr, (uint32_t)(64 * g + 16 * kg + r16) * 4u, 0, 0))
-                       : 1.0f;
+        if constexpr (FP4) {
+            G.ks[0] = k_scale ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                          ksr, (uint32_t)(64 * g + 16 * kg + r16) * 4u, 0, 0))
+                              : 1.0f;
+        } else {
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj)
+                G.ks[jj] = k_scale ? __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+                                                               ksr, (uint32_t)(64 * g + 16 * jj + r16) * 4u, 0, 0))
+                                   : 1.0f;
+        }
     };
     auto compute = [&](int g, const Group &G) {
-        // one vector per token, so that picking this lane's key below is a
-        // register select (an array of floats picked by kg goes to scratch)
-        v4f res[NQ];
-        // (fp8 serves decode only: a group past every limit is rare there)
-        const bool masked = FP4 && c0 + 64 * g > last_lim;  // block-uniform
+        if constexpr (!FP4) {
+            // per 16-key block: the tokens' head groups accumulate into one
+            // head-sum result, lane group t holding token t's scores; one
+            // store writes them all
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const v8i bk = FP4 ? expand_e2m1(G.k[j])
-                               : v8i{G.k[2 * j][0], G.k[2 * j][1], G.k[2 * j][2], G.k[2 * j][3],
-                                     G.k[2 * j + 1][0], G.k[2 * j + 1][1], G.k[2 * j + 1][2], G.k[2 * j + 1][3]};
+            for (int j = 0; j < 4; ++j) {
+                const v8i bk = v8i{G.k[2 * j][0], G.k[2 * j][1], G.k[2 * j][2], G.k[2 * j][3],
+                                   G.k[2 * j + 1][0], G.k[2 * j + 1][1], G.k[2 * j + 1][2], G.k[2 * j + 1][3]};
+                v4f hc;
+                head_sum_group<true>(hc, a[0][0], a[0][1], a[0][2], a[0][3], bk, IDX_MFMA_SCALES, wA[0][0], wA[0][1]);
 #pragma unroll
-            for (int t = 0; t < NQ; ++t) {
-                // block-uniform; a masked group's stores write -inf, a
-                // missing token's none
-                if (t >= nv || masked)
-                    continue;
-                float r;
-                if constexpr (FP4)
+                for (int t = 1; t < NQ; ++t) {
+                    if (t >= nv)  // block-uniform; a missing token's lanes store nothing
+                        continue;
+                    head_sum_group<false>(hc, a[t][0], a[t][1], a[t][2], a[t][3], bk, IDX_MFMA_SCALES, wA[t][0],
+                                          wA[t][1]);
+                }
+                const int s = c0 + 64 * g + 16 * j + r16;  // the key this lane stores, for token kg
+                const float v = s > lane_lim ? -INFINITY : hc[0] * G.ks[j];
+                const uint32_t off = (kg < nv && s < ctx) ? (uint32_t)(kg * ctx + s) * 4u : 0x80000000u;
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), srs, off, 0, 0);
+            }
+        } else {
+            // one vector per token, so that picking this lane's key below is a
+            // register select (an array of floats picked by kg goes to scratch)
+            v4f res[NQ];
+            const bool masked = c0 + 64 * g > last_lim;  // block-uniform
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const v8i bk = expand_e2m1(G.k[j]);
+#pragma unroll
+                for (int t = 0; t < NQ; ++t) {
+                    // block-uniform; a masked group's stores write -inf, a
+                    // missing token's none
+                    if (t >= nv || masked)
+                        continue;
+                    float r;
                     head_group_f4<true>(r, a[t][0], a[t][1], a[t][2], a[t][3], bk, F4_QUERY_SCALE, G.bs[j],
                                         &wv[t][0]);
-                else
-                    head_group<true>(r, a[t][0], a[t][1], a[t][2], a[t][3], bk, IDX_MFMA_SCALES, &wv[t][0]);
-                r += xor_lanes16(r);
-                r += __shfl_xor(r, 32, 64);
-                res[t][j] = r;
+                    r += xor_lanes16(r);
+                    r += __shfl_xor(r, 32, 64);
+                    res[t][j] = r;
+                }
             }
-        }
-        const int s = c0 + 64 * g + 16 * kg + r16;  // the key this lane stores
+            const int s = c0 + 64 * g + 16 * kg + r16;  // the key this lane stores
 #pragma unroll
-        for (int t = 0; t < NQ; ++t) {
-            if (t >= nv)
-                continue;
-            float v = res[t][kg];
-            v = s > lim[t] ? -INFINITY : v * G.ks;
-            const uint32_t off = s < ctx ? (uint32_t)(t * ctx + s) * 4u : 0x80000000u;
-            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), srs, off, 0, 0);
+            for (int t = 0; t < NQ; ++t) {
+                if (t >= nv)
+                    continue;
+                float v = res[t][kg];
+                v = s > lim[t] ? -INFINITY : v * G.ks[0];
+                const uint32_t off = s < ctx ? (uint32_t)(t * ctx + s) * 4u : 0x80000000u;
+                __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), srs, off, 0, 0);
+            }
         }
     };
     // The prefetch is unconditional (groups past the chunk read zeros through
