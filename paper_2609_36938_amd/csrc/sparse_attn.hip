@@ -526,13 +526,24 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // the common case - every key of the tile valid, bf16 rows and a
         // positive scale - takes the max over the raw products and one fma
         // per probability, with no masks
-        const bool fast = !KV8 && vbits == 0xFFFFFFFFu && scale_log2 > 0.f;
+        const bool fast = vbits == 0xFFFFFFFFu && scale_log2 > 0.f;
         // fp8 rows: each key's scale (ks, read from step KS_STEP on)
         // multiplies its logit and its probability
         float x[2][4];
         float mx = -INFINITY;
         if (fast) {
-            mx = scale_log2 * max8(st0, st1);
+            if constexpr (KV8) {
+                // fp8 rows: no masks, each logit times its key's scale
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    x[0][i] = st0[i] * (scale_log2 * ks[0][i]);
+                    x[1][i] = st1[i] * (scale_log2 * ks[1][i]);
+                }
+                mx = fmaxf(fmaxf(fmaxf(x[0][0], x[0][1]), fmaxf(x[0][2], x[0][3])),
+                           fmaxf(fmaxf(x[1][0], x[1][1]), fmaxf(x[1][2], x[1][3])));
+            } else {
+                mx = scale_log2 * max8(st0, st1);
+            }
         } else {
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb)
@@ -572,8 +583,14 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    pv[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(kb ? st1[i] : st0[i], scale_log2, -m));
-                    lsum += pv[kb][i];
+                    if constexpr (KV8) {
+                        pv[kb][i] = __builtin_amdgcn_exp2f(x[kb][i] - m);
+                        lsum += pv[kb][i];
+                        pv[kb][i] *= ks[kb][i];  // V_s = scale_s * (stored row)
+                    } else {
+                        pv[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(kb ? st1[i] : st0[i], scale_log2, -m));
+                        lsum += pv[kb][i];
+                    }
                 }
         } else {
 #pragma unroll
