@@ -44,7 +44,6 @@ constexpr int MLA_CPR = MLA_DQK * 2 / 16;      // 16-byte chunks per cached row 
 constexpr int MLA_PCH = MLA_CPR + 2;            // LDS row pitch in chunks: 1184 B reads the K operand conflict-free
 constexpr int MLA_ROWB = MLA_PCH * 16;          // LDS bytes per tile row
 constexpr int MLA_TILE_CH = MLA_KT * MLA_PCH;   // chunks per tile (2368)
-constexpr int MLA_TILE_INS = (MLA_TILE_CH + 63) / 64;  // wave-instructions per tile (37)
 constexpr int MLA_MAX_K = 4096;                 // selected ids per token held in LDS
 constexpr float RESCALE_SLACK = 8.0f;           // log2 headroom before O is rescaled
 // Running max before any valid logit: finite and below every logit, so that
