@@ -77,6 +77,26 @@ def test_index_scores_parity_ragged(dt, H, d, tol):
     _score_check(wl, _rows_of(sc.cpu().numpy(), wl), tol)
 
 
+@pytest.mark.parametrize("hist,new", [([4200, 1500, 0], [37, 20, 10]), ([9000, 300, 64], [1, 3, 2])])
+def test_fp8_index_scores_without_scales(hist, new):
+    """fp8 keys and queries with both scale arrays NULL (every scale 1): the
+    prefill kernel (sessions appending more than 4 tokens) and the row-tile
+    kernel (at most 4), against the oracle over the same bytes."""
+    wl = make_workload(hist_len=hist, new_len=new, H=64, d=128, idx_dtype="fp8", k=16, seed=37, w_scale=0.125)
+    bt = _batch(wl)
+    sc = janus.index_scores(bt, T(wl.q), T(wl.kI), T(wl.w), q_scale=None, k_scale=None, dtype="fp8")
+    torch.cuda.synchronize()
+    got = _rows_of(sc.cpu().numpy(), wl)
+    rows = np.arange(wl.total_q)
+    ref = oracle.index_scores(wl.q_start, wl.hist_len, wl.q, "fp8", None, wl.kI, "fp8", None, wl.w, rows,
+                              out_ld=wl.max_ctx)
+    fin = np.isfinite(ref)
+    assert np.array_equal(fin, np.isfinite(got))
+    diff = np.where(fin, np.abs(got.astype(np.float64) - np.where(fin, ref, 0.0)), 0.0)
+    scale = np.where(fin, np.abs(ref), 0.0).max(axis=1)
+    assert (diff.max(axis=1) <= 1e-2 * np.maximum(scale, 1e-300)).all()
+
+
 def _topk_case(hist, new, k, fill, seed=0):
     """A batch plus a synthetic flat score buffer built by `fill(rng, b, i, n)`."""
     rng = np.random.default_rng(seed)
