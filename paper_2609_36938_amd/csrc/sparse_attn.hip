@@ -257,13 +257,15 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         const int s = sel[j];
         sSlot[j] = (s >= 0 && s <= lim) ? ((pt[s >> page_shift] << page_shift) + (s & psz_mask)) : -1;
     }
-    // queries of head head0 + c16, dims 32*step + 8*grp .. +7
+    // queries of head head0 + c16: bf16 rows, dims 32*step + 8*grp .. +7;
+    // fp8 rows, steps in pairs (2p, 2p+1) over dims 64p + 16*grp .. +15, the
+    // first 8 for step 2p, so that one 16-byte K read serves both steps
     v8bf qf[MLA_STEPS];
     {
-        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + c16) * MLA_DQK + 8 * grp;
+        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + c16) * MLA_DQK + (KV8 ? 16 : 8) * grp;
 #pragma unroll
         for (int st = 0; st < MLA_STEPS; ++st)
-            qf[st] = as_v8bf(*(const v4i *)(qr + 32 * st));
+            qf[st] = as_v8bf(*(const v4i *)(qr + (KV8 ? 64 * (st / 2) + 8 * (st % 2) : 32 * st)));
     }
     // O for all HQ heads (head block hb = rows 16*hb .. 16*hb+15) over this
     // wave's NBW blocks of 16 output dims, dims 16*(NBW*wave + nl) + c16
@@ -479,16 +481,36 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                 return *(const KRaw *)(tile + tail_off((lnk & 15) + 16 * h, 4 * (step - 16) + (lnk >> 4)));
             return *(const KRaw *)((h ? row1 : row0) + SB * step);
         };
-        // two steps ahead: a three-entry ring
+        // two steps ahead: a three-entry ring (fp8 rows: a two-entry ring
+        // of step pairs, each 16-byte read holding two steps' operands)
         constexpr int AHEAD = 2;
         KRaw ring[AHEAD + 1][2];
+        v4i pring[2][2];
+        const uint8_t *prow0 = tile + kv8_key_off(c16) + 16 * grp, *prow1 = tile + kv8_key_off(c16 + 16) + 16 * grp;
+        if constexpr (KV8) {
+            pring[0][0] = *(const v4i *)prow0;
+            pring[0][1] = *(const v4i *)prow1;
+        } else {
 #pragma unroll
-        for (int a = 0; a < AHEAD; ++a) {
-            ring[a][0] = kop(a, 0);
-            ring[a][1] = kop(a, 1);
+            for (int a = 0; a < AHEAD; ++a) {
+                ring[a][0] = kop(a, 0);
+                ring[a][1] = kop(a, 1);
+            }
         }
 #pragma unroll
         for (int step = 0; step < MLA_STEPS; ++step) {
+            if constexpr (KV8) {
+                const int pp = step / 2;
+                if (step % 2 == 0 && pp + 1 < MLA_STEPS / 2) {
+                    pring[(pp + 1) & 1][0] = *(const v4i *)(prow0 + 64 * (pp + 1));
+                    pring[(pp + 1) & 1][1] = *(const v4i *)(prow1 + 64 * (pp + 1));
+                }
+                const v4i k0 = pring[pp & 1][0], k1 = pring[pp & 1][1];
+                const v2i h0 = step % 2 ? v2i{k0[2], k0[3]} : v2i{k0[0], k0[1]};
+                const v2i h1 = step % 2 ? v2i{k1[2], k1[3]} : v2i{k1[0], k1[1]};
+                st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(h0), qf[step], st0, 0, 0, 0);
+                st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(h1), qf[step], st1, 0, 0, 0);
+            } else {
             if (step + AHEAD < MLA_STEPS) {
                 ring[(step + AHEAD) % (AHEAD + 1)][0] = kop(step + AHEAD, 0);
                 ring[(step + AHEAD) % (AHEAD + 1)][1] = kop(step + AHEAD, 1);
@@ -497,6 +519,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                                                           0);
             st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step % (AHEAD + 1)][1]), qf[step], st1, 0, 0,
                                                           0);
+            }
             // issue points: fp8 at steps 0, 4, .., 16; bf16 at 2, 6, 10, 14
             // and 17, after the slots read at the top of the tile have landed
             if (KV8 ? step % 4 == 0 : (step % 4 == 2 || step == MLA_STEPS - 1))
