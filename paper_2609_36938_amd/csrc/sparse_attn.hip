@@ -138,9 +138,14 @@ constexpr int KV8_GAP = 8;                               // chunks between keys 
 constexpr int KV8_TILE_CH = MLA_KT * KV8_CPR + KV8_GAP;  // 1192
 constexpr int KV8_SCALE = MLA_DQK;                       // byte of the scale in a row
 JANUS_DEV int kv8_key_off(int r) { return r * KV8_ROWB + (r >= 16 ? KV8_GAP * 16 : 0); }
-// K-step at which a tile's key scales are read (their LDS latency passes
-// under the remaining steps; at the last step it showed in the softmax)
-constexpr int KS_STEP = 10;
+// fp8 rows: K-step at which a tile's key scales are read (their LDS latency
+// passes under the remaining steps; at the last step it showed in the softmax)
+constexpr int KS_STEP = 4;
+// fp8 rows: S^T = K Q^T on the fp8 MFMA (16x16x128), in five K-steps: dims
+// 128c .. 128c+127 for c < 4 (lane group grp holds dims 128c + 32grp .. +31),
+// then the 64 tail dims, whose MFMA takes the high parts of the queries in
+// lane groups 0-1 and the low parts in groups 2-3 against the same key bytes
+constexpr int KV8_STEPS = 5;
 
 // bf16 rows in a tile buffer: dims 0..511 of key row r ("main", 1 KB) at
 // r * MLA_ROWB, so that one gather instruction loads one row and its source
@@ -191,6 +196,47 @@ JANUS_DEV void tile_chunk_j(int j, int lane, int &r, int &c)
 }
 
 // 8 fp8 e4m3 values -> 8 bf16 (exact: e4m3 values are bf16 values)
+JANUS_DEV v8bf fp8x8_to_bf16(v2i x);
+
+// four fp32 values -> four fp8 e4m3 bytes (round to nearest even); the
+// values are within the format's range
+JANUS_DEV int fp8x4_of(float a, float b, float c, float d)
+{
+    v2s w = {0, 0};
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, a, b, 1.0f, false);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, c, d, 1.0f, true);
+    return __builtin_bit_cast(int, w);
+}
+
+// 32 bf16 query values (four 16-byte words) times inv, split into two fp8
+// parts, hi + lo == x * inv exactly for |x * inv| < 256 and |x * inv| >= 2^-2
+// (hi keeps the 4 leading significant bits of the 8, lo the remaining 4);
+// smaller values lose at most 2^-10 to the underflow of lo
+JANUS_DEV void split_fp8x32(const v4i (&x)[4], float inv, v8i &hi, v8i &lo)
+{
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int w0 = x[u][2 * h], w1 = x[u][2 * h + 1];
+            const float f0 = __builtin_bit_cast(float, w0 << 16) * inv;
+            const float f1 = __builtin_bit_cast(float, w0 & (int)0xffff0000) * inv;
+            const float f2 = __builtin_bit_cast(float, w1 << 16) * inv;
+            const float f3 = __builtin_bit_cast(float, w1 & (int)0xffff0000) * inv;
+            const int hw = fp8x4_of(f0, f1, f2, f3);
+            const v2f b01 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(hw, 1.0f, false);
+            const v2f b23 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(hw, 1.0f, true);
+            hi[2 * u + h] = hw;
+            lo[2 * u + h] = fp8x4_of(f0 - b01[0], f1 - b01[1], f2 - b23[0], f3 - b23[1]);
+        }
+}
+
+// S^T += K Q^T over 128 dims on fp8 operands (E8M0 scales 1)
+JANUS_DEV v4f mfma_fp8x128(v8i a, v8i b, v4f c)
+{
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
 JANUS_DEV v8bf fp8x8_to_bf16(v2i x)
 {
     const v2bf a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(x[0], 1.0f, false);
@@ -231,6 +277,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
     __shared__ float sAlpha[HQ];     // O rescale factor per head this tile
     __shared__ int32_t sResc[NW];    // wave w's heads were rescaled this tile
     __shared__ float sInvL[HQ];      // 1 / softmax denominator per head
+    __shared__ v8i sQT[KV8 ? NW * 64 : 1];  // fp8 rows: the tail K-step's query operand, wave w's lane l at 64w + l
 
     // SPLIT: block (g, sp) is token g, slice sp of its selection (whole
     // tiles); otherwise block g is token g over its whole selection
@@ -257,15 +304,68 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         const int s = sel[j];
         sSlot[j] = (s >= 0 && s <= lim) ? ((pt[s >> page_shift] << page_shift) + (s & psz_mask)) : -1;
     }
-    // queries of head head0 + c16: bf16 rows, dims 32*step + 8*grp .. +7;
-    // fp8 rows, steps in pairs (2p, 2p+1) over dims 64p + 16*grp .. +15, the
-    // first 8 for step 2p, so that one 16-byte K read serves both steps
-    v8bf qf[MLA_STEPS];
-    {
-        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + c16) * MLA_DQK + (KV8 ? 16 : 8) * grp;
+    // queries of head head0 + c16.  bf16 rows: dims 32*step + 8*grp .. +7.
+    // fp8 rows: q = s * (hi + lo) with hi and lo fp8 and s a power of two per
+    // head (max |q| / s < 256), so that S^T runs on the fp8 MFMA straight
+    // from the stored key bytes; qf[c] and qf[4 + c] hold hi and lo of dims
+    // 128c + 32grp .. +31, and sQT the tail (dims 512 + 32(grp & 1) .. +31:
+    // hi in lane groups 0-1, lo in 2-3), read back at each tile's tail step
+    // (its registers are what the kernel lacks).  The split is exact for
+    // every value above 2^-10 of its head's largest and loses at most
+    // 2^-18 of that largest below, so a logit is within 576 * 2^-18 *
+    // max|q| * max|k| (under 2^-8.8 of their product) of q.k, beside fp32
+    // rounding
+    using QReg = std::conditional_t<KV8, v8i, v8bf>;
+    QReg qf[KV8 ? 8 : MLA_STEPS];
+    float ksc = scale_log2;  // logit scale (fp8 rows: times s)
+    if constexpr (KV8) {
+        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + c16) * MLA_DQK;
+        auto qword = [&](int c, int u) {
+            return *(const v4i *)(qr + (c < 4 ? 128 * c + 32 * grp : MLA_DV + 32 * (grp & 1)) + 8 * u);
+        };
+        // max |q| over the head: lanes c16 + 16 * grp (finite bf16
+        // magnitudes order as integers);
+        // the words are read again for the split, one step at a time, so
+        // that they are never all held in registers
+        int mlo = 0, mhi = 0;
+#pragma unroll
+        for (int c = 0; c < 5; ++c)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const v4i w = qword(c, u);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    mlo = max(mlo, w[e] & 0x7fff);
+                    mhi = max(mhi, (int)((uint32_t)w[e] >> 16) & 0x7fff);
+                }
+            }
+        asm volatile("" ::: "memory");
+        int mq = max(mlo, mhi);
+#pragma unroll
+        for (int off = 16; off <= 32; off <<= 1)
+            mq = max(mq, __shfl_xor(mq, off));
+        int ex;
+        (void)frexpf(__builtin_bit_cast(float, mq << 16), &ex);  // max |q| < 2^ex
+        ex = min(max(ex, -100), 120);
+        const float inv = ldexpf(1.0f, 8 - ex);
+        ksc = scale_log2 * ldexpf(1.0f, ex - 8);
+#pragma unroll
+        for (int c = 0; c < 5; ++c) {
+            const v4i raw[4] = {qword(c, 0), qword(c, 1), qword(c, 2), qword(c, 3)};
+            if (c < 4) {
+                split_fp8x32(raw, inv, qf[c], qf[4 + c]);
+            } else {
+                v8i th, tl;
+                split_fp8x32(raw, inv, th, tl);
+                sQT[64 * wave + lane] = grp < 2 ? th : tl;
+            }
+            __builtin_amdgcn_sched_barrier(0);
+        }
+    } else {
+        const uint16_t *qr = q + ((int64_t)g * HQ + head0 + c16) * MLA_DQK + 8 * grp;
 #pragma unroll
         for (int st = 0; st < MLA_STEPS; ++st)
-            qf[st] = as_v8bf(*(const v4i *)(qr + (KV8 ? 64 * (st / 2) + 8 * (st % 2) : 32 * st)));
+            qf[st] = as_v8bf(*(const v4i *)(qr + 32 * st));
     }
     // O for all HQ heads (head block hb = rows 16*hb .. 16*hb+15) over this
     // wave's NBW blocks of 16 output dims, dims 16*(NBW*wave + nl) + c16
@@ -447,27 +547,21 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         float ks[2][4];  // fp8 rows: scales of keys 16*kb + 4*grp + i
         // S^T[key][head] = K Q^T for keys 16*kb + 4*grp + i
         v4f st0 = v4f{0.f, 0.f, 0.f, 0.f}, st1 = st0;
-        // K operands: 16 bytes (bf16) or 8 bytes (fp8, widened to bf16 in
-        // registers) per lane and K-step for keys c16 and c16 + 16.  Q and O
-        // fill most of the registers, so the compiler alone keeps too few
-        // operand reads in flight: each step loads the operands of the step
-        // two ahead into a ring, and a scheduling fence per step keeps it from
-        // hoisting more than that.  The ring keeps its reads in flight only
-        // because the gathers are assembly (gather16): after the builtin the
-        // compiler waits for every outstanding LDS read
-        using KRaw = std::conditional_t<KV8, v2i, v4i>;
-        constexpr int SB = KV8 ? 32 : 64;  // bytes per K-step
-        const uint8_t *row0 = KV8 ? tile + kv8_key_off(c16) + 8 * grp : tile + c16 * MLA_ROWB + 16 * grp;
-        const uint8_t *row1 = KV8 ? tile + kv8_key_off(c16 + 16) + 8 * grp : row0 + 16 * MLA_ROWB;
-        auto widen = [](KRaw x) {
-            if constexpr (KV8)
-                return fp8x8_to_bf16(x);
-            else
-                return as_v8bf(x);
-        };
+        // K operands for keys c16 and c16 + 16: bf16 rows, 16 bytes per lane
+        // and K-step; fp8 rows, 32 (the key bytes themselves).  Q and O fill
+        // most of the registers, so the compiler alone keeps too few operand
+        // reads in flight: each step loads the operands of a later step into
+        // a ring (bf16 two steps ahead, fp8 one), and a scheduling fence per
+        // step keeps it from hoisting more than that.  The ring keeps its
+        // reads in flight only because the gathers are assembly (gather16):
+        // after the builtin the compiler waits for every outstanding LDS read
+        using KRaw = v4i;
+        constexpr int SB = 64;  // bytes per K-step
+        const uint8_t *row0 = tile + c16 * MLA_ROWB + 16 * grp;
+        const uint8_t *row1 = row0 + 16 * MLA_ROWB;
         // fp8 rows: the waves raise their priority over the MFMA loops, so
-        // that a wave still in them is issued ahead of one in the widening
-        // or softmax VALU work (measured 3% faster; no gain with bf16 rows)
+        // that a wave still in them is issued ahead of one in the softmax
+        // or P·V VALU work
         if constexpr (KV8)
             __builtin_amdgcn_s_setprio(1);
         // K operand of a step for keys c16 (h = 0) and c16 + 16 (h = 1): bf16
@@ -485,11 +579,27 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
         // of step pairs, each 16-byte read holding two steps' operands)
         constexpr int AHEAD = 2;
         KRaw ring[AHEAD + 1][2];
-        v4i pring[2][2];
-        const uint8_t *prow0 = tile + kv8_key_off(c16) + 16 * grp, *prow1 = tile + kv8_key_off(c16 + 16) + 16 * grp;
+        // fp8 rows: key bytes of K-step c (tail: lane groups 2-3 repeat the
+        // bytes of groups 0-1).  Operand j = 2c + h (keys c16 + 16h) lives in
+        // kring[j % 3]: a step's first MFMAs find the next step's keys c16
+        // loaded, and each operand's register is refilled after its last MFMA
+        const uint8_t *arow0 = tile + kv8_key_off(c16) + 32 * grp, *arow1 = tile + kv8_key_off(c16 + 16) + 32 * grp;
+        const int tail8 = MLA_DV + 32 * (grp & 1) - 32 * grp;
+        auto kop8 = [&](int c, int h) -> v8i {
+            // an opaque offset keeps each read in its step (the compiler
+            // otherwise hoists them all to the top of the tile)
+            int o = c < 4 ? 128 * c : tail8;
+            asm volatile("" : "+v"(o));
+            const uint8_t *p = (h ? arow1 : arow0) + o;
+            const v4i a = *(const v4i *)p, b = *(const v4i *)(p + 16);
+            return v8i{a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+        };
+        v8i kring[3], qtail;
+        constexpr int NSTEP = KV8 ? KV8_STEPS : MLA_STEPS;
         if constexpr (KV8) {
-            pring[0][0] = *(const v4i *)prow0;
-            pring[0][1] = *(const v4i *)prow1;
+            kring[0] = kop8(0, 0);
+            kring[1] = kop8(0, 1);
+            kring[2] = kop8(1, 0);
         } else {
 #pragma unroll
             for (int a = 0; a < AHEAD; ++a) {
@@ -498,34 +608,41 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             }
         }
 #pragma unroll
-        for (int step = 0; step < MLA_STEPS; ++step) {
+        for (int step = 0; step < NSTEP; ++step) {
             if constexpr (KV8) {
-                const int pp = step / 2;
-                if (step % 2 == 0 && pp + 1 < MLA_STEPS / 2) {
-                    pring[(pp + 1) & 1][0] = *(const v4i *)(prow0 + 64 * (pp + 1));
-                    pring[(pp + 1) & 1][1] = *(const v4i *)(prow1 + 64 * (pp + 1));
+                const int j0 = 2 * step;
+                if (step == 3)
+                    qtail = sQT[64 * wave + lnk];
+                const v8i qa = step < 4 ? qf[step] : qtail;
+                st0 = mfma_fp8x128(kring[j0 % 3], qa, st0);
+                st1 = mfma_fp8x128(kring[(j0 + 1) % 3], qa, st1);
+                if (step < 4) {
+                    st0 = mfma_fp8x128(kring[j0 % 3], qf[4 + step], st0);
+                    kring[j0 % 3] = kop8(step + 1, 1);
+                    st1 = mfma_fp8x128(kring[(j0 + 1) % 3], qf[4 + step], st1);
+                    if (step + 2 < NSTEP)
+                        kring[(j0 + 1) % 3] = kop8(step + 2, 0);
                 }
-                const v4i k0 = pring[pp & 1][0], k1 = pring[pp & 1][1];
-                const v2i h0 = step % 2 ? v2i{k0[2], k0[3]} : v2i{k0[0], k0[1]};
-                const v2i h1 = step % 2 ? v2i{k1[2], k1[3]} : v2i{k1[0], k1[1]};
-                st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(h0), qf[step], st0, 0, 0, 0);
-                st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fp8x8_to_bf16(h1), qf[step], st1, 0, 0, 0);
+                // a use of the products here keeps the MFMAs in their step:
+                // the compiler otherwise sinks them all past the branches of
+                // the gather issue, holding every step's key operands at once
+                asm volatile("" ::"v"(st0), "v"(st1));
             } else {
             if (step + AHEAD < MLA_STEPS) {
                 ring[(step + AHEAD) % (AHEAD + 1)][0] = kop(step + AHEAD, 0);
                 ring[(step + AHEAD) % (AHEAD + 1)][1] = kop(step + AHEAD, 1);
             }
-            st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step % (AHEAD + 1)][0]), qf[step], st0, 0, 0,
+            st0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(ring[step % (AHEAD + 1)][0]), qf[step], st0, 0, 0,
                                                           0);
-            st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(widen(ring[step % (AHEAD + 1)][1]), qf[step], st1, 0, 0,
+            st1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_v8bf(ring[step % (AHEAD + 1)][1]), qf[step], st1, 0, 0,
                                                           0);
             }
-            // issue points: fp8 at steps 0, 4, .., 16; bf16 at 2, 6, 10, 14
-            // and 17, after the slots read at the top of the tile have landed
-            if (KV8 ? step % 4 == 0 : (step % 4 == 2 || step == MLA_STEPS - 1))
-                issue_part(t, KV8 ? step / 4 : (step == MLA_STEPS - 1 ? 4 : step / 4), vs, ts, next);
+            // issue points: fp8 at every step; bf16 at 2, 6, 10, 14 and 17,
+            // after the slots read at the top of the tile have landed
+            if (KV8 || step % 4 == 2 || step == MLA_STEPS - 1)
+                issue_part(t, KV8 ? step : (step == MLA_STEPS - 1 ? 4 : step / 4), vs, ts, next);
             // this tile's slots (for its valid keys), read under the last MFMAs
-            if (step == MLA_STEPS - 1)
+            if (step == NSTEP - 1)
                 vslot = sSlot[min(MLA_KT * t + (lane & 31), kl - 1)];
             if constexpr (KV8) {
                 if (step == KS_STEP) {
@@ -558,8 +675,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
                 // fp8 rows: no masks, each logit times its key's scale
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    x[0][i] = st0[i] * (scale_log2 * ks[0][i]);
-                    x[1][i] = st1[i] * (scale_log2 * ks[1][i]);
+                    x[0][i] = st0[i] * (ksc * ks[0][i]);
+                    x[1][i] = st1[i] * (ksc * ks[1][i]);
                 }
                 mx = fmaxf(fmaxf(fmaxf(x[0][0], x[0][1]), fmaxf(x[0][2], x[0][3])),
                            fmaxf(fmaxf(x[1][0], x[1][1]), fmaxf(x[1][2], x[1][3])));
@@ -572,7 +689,7 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const bool ok = (vmask >> (16 * kb + i)) & 1u;
-                    const float sc = KV8 ? scale_log2 * ks[kb][i] : scale_log2;
+                    const float sc = KV8 ? ksc * ks[kb][i] : scale_log2;
                     x[kb][i] = ok ? (kb ? st1[i] : st0[i]) * sc : -INFINITY;
                     mx = fmaxf(mx, x[kb][i]);
                 }
