@@ -11,7 +11,7 @@ import pytest
 import torch
 
 import oracle
-from workloads import attention_inputs, attention_kv_fp8, attention_q_rows, make_workload, synth_topk
+from workloads import attention_inputs, attention_kv_fp8, attention_q_rows, make_workload, synth_topk, to_bf16_bits
 from workloads.gen import MLA_ATTN
 
 pytestmark = pytest.mark.gpu
@@ -77,4 +77,38 @@ def test_mla_fp8_heads(case, splits):
     rows = np.arange(wl.total_q, dtype=np.int32)
     ref, lref = oracle.sparse_attn_fp8kv(wl.q_start, wl.hist_len, rows, attention_q_rows(wl, rows), pool8,
                                          wl.page_table, wl.page_size, sel[rows], ai.scale, entry=1)
+    _compare(out.cpu().numpy(), lse.cpu().numpy(), ref, lref)
+
+
+def test_mla_fp8_wide_query_range():
+    """fp8 rows, 128 heads, with queries whose heads' scales differ by up to
+    2^6 within a wave and whose elements are standard normal draws times
+    2^u, u uniform over -8..0, at a logit scale (4) that makes the softmax of
+    most heads peaked (lse up to about 36).  The fp8 kernel splits each
+    head's query into two fp8 parts under a power-of-two scale of its own;
+    the split is exact above 2^-10 of the head's largest element and loses
+    at most 2^-18 of it below, so a logit is within 576 * 2^-18 * max|q| *
+    max|k| of q.k.  Here that stays inside the usual tolerances; at a logit
+    scale of 16 the same inputs reach lse errors of about 2e-3 at lse ~ 135,
+    and elements spread over 30 binades inside one head reach 2.4e-3.
+    Against the oracle on every row."""
+    attn = dict(MLA_ATTN, Hq=128, kv_std=1.0 / 24.0, scale=4.0)
+    wl = make_workload(hist_len=[1500, 300], new_len=[6, 5], H=2, d=8, idx_dtype="f32", k=200, seed=77,
+                       table="permuted", attn=attn)
+    sel = synth_topk(wl, seed=5, pad_rows=2)
+    ai = attention_inputs(wl)
+    rng = np.random.default_rng(13)
+    qf = (ai.q.astype(np.uint32) << 16).view(np.float32)
+    e = rng.integers(-8, 1, size=qf.shape).astype(np.float32)
+    hs = (np.arange(qf.shape[1]) % 7 - 3).astype(np.float32)[None, :, None]
+    qf = qf * np.exp2(e + hs)
+    qb = to_bf16_bits(qf.astype(np.float32))
+    pool8 = attention_kv_fp8(wl)
+    bt = janus.Batch(wl.hist_len, wl.new_len)
+    out, lse = janus.sparse_attn_fp8kv(bt, T(qb), T(pool8), T(wl.page_table), wl.page_size, T(sel), ai.scale,
+                                       out_dtype="f32", want_lse=True)
+    torch.cuda.synchronize()
+    rows = np.arange(wl.total_q, dtype=np.int32)
+    ref, lref = oracle.sparse_attn_fp8kv(wl.q_start, wl.hist_len, rows, qb, pool8, wl.page_table, wl.page_size,
+                                         sel[rows], ai.scale, entry=1)
     _compare(out.cpu().numpy(), lse.cpu().numpy(), ref, lref)
