@@ -139,8 +139,8 @@ constexpr int KV8_TILE_CH = MLA_KT * KV8_CPR + KV8_GAP;  // 1192
 constexpr int KV8_SCALE = MLA_DQK;                       // byte of the scale in a row
 JANUS_DEV int kv8_key_off(int r) { return r * KV8_ROWB + (r >= 16 ? KV8_GAP * 16 : 0); }
 // fp8 rows: K-step at which a tile's key scales are read (their LDS latency
-// passes under the remaining steps; at the last step it showed in the softmax)
-constexpr int KS_STEP = 4;
+// passes under the remaining steps; at step 4, the last, 1.3% slower)
+constexpr int KS_STEP = 3;
 // fp8 rows: S^T = K Q^T on the fp8 MFMA (16x16x128), in five K-steps: dims
 // 128c .. 128c+127 for c < 4 (lane group grp holds dims 128c + 32grp .. +31),
 // then the 64 tail dims, whose MFMA takes the high parts of the queries in
