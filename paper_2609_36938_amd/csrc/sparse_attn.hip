@@ -642,8 +642,8 @@ __global__ __launch_bounds__(64 * NW, 1) void sparse_mla_mfma(
             if (KV8 || step % 4 == 2 || step == MLA_STEPS - 1)
                 issue_part(t, KV8 ? step : (step == MLA_STEPS - 1 ? 4 : step / 4), vs, ts, next);
             // this tile's slots (for its valid keys), read under the last
-            // MFMAs (fp8 rows: the last two steps)
-            if (step == (KV8 ? NSTEP - 2 : NSTEP - 1))
+            // MFMAs (bf16 rows: the last three steps, fp8 rows: two)
+            if (step == (KV8 ? NSTEP - 2 : NSTEP - 3))
                 vslot = sSlot[min(MLA_KT * t + (lane & 31), kl - 1)];
             if constexpr (KV8) {
                 if (step == KS_STEP) {
